@@ -1,0 +1,170 @@
+"""CPU oracle for the tree-verification step (arXiv 2603.01639, section 3.2).
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  It wraps the plain
+fp64 C library ``libltdoracle.so`` (``ltd_oracle.c``) with numpy-array calls.
+It shares no code with the HIP library, and the HIP library never reaches it.
+
+Every function takes host numpy arrays in the same layouts as the GPU contract:
+
+* ``q``: ``[B][Nmax][Hq][d]``, float32 or bf16 bit patterns (uint16);
+* ``k_cache``/``v_cache``: contiguous ``[B][Hkv][cap][d]`` or paged
+  ``[num_blocks][Hkv][block_size][d]`` with ``block_table`` ``[B][max_blocks]``;
+* ``parents``: ``[B][Nmax]`` int32 with ``parents[b][0] == -1``.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libltdoracle.so")
+
+DTYPE_F32 = 0
+DTYPE_BF16 = 1
+
+STATUS_BAD_NNODES = 1
+STATUS_BAD_PARENT = 2
+STATUS_BAD_PREFIX = 3
+STATUS_BAD_BLOCK = 4
+STATUS_BAD_PATH = 5
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code):
+        super().__init__(f"oracle returned {code}")
+        self.code = code
+
+
+_lib = None
+
+
+def load_library(path: str) -> ctypes.CDLL:
+    """Open an oracle build at ``path`` and declare its signatures."""
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    i32 = ctypes.c_int
+    lib.ltd_oracle_tree_verify_attn.argtypes = [P, P, P, P, P, P, P, P, P, i32, i32, i32, i32,
+                                                i32, i32, i32, i32, ctypes.c_double, i32]
+    lib.ltd_oracle_tree_verify_attn.restype = i32
+    lib.ltd_oracle_tree_accept.argtypes = [P, P, P, P, i32, i32, i32, P, P, P, P]
+    lib.ltd_oracle_tree_accept.restype = i32
+    lib.ltd_oracle_kv_compact.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32, i32,
+                                          i32, i32, ctypes.c_int64, i32]
+    lib.ltd_oracle_kv_compact.restype = i32
+    lib.ltd_oracle_num_threads.argtypes = []
+    lib.ltd_oracle_num_threads.restype = i32
+    return lib
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            from . import build as _build
+            _build.build()
+        _lib = load_library(LIB_PATH)
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return None if a is None else np.ascontiguousarray(a, dtype=dtype)
+
+
+def num_threads() -> int:
+    return int(_load().ltd_oracle_num_threads())
+
+
+def tree_verify_attn(q, k_cache, v_cache, prefix_len, parents, n_nodes, *, Hkv, block_table=None,
+                     num_blocks=0, scale=None, dtype=DTYPE_BF16, out=None, node_mask=None):
+    """fp64 tree attention.  Returns ``out`` ``[B][Nmax][Hq][d]`` float64.
+
+    Rows ``i >= n_nodes[b]`` (and rows outside ``node_mask`` when it is given)
+    are left as they were in ``out`` (zeros if not given).
+    """
+    lib = _load()
+    elem = np.float32 if dtype == DTYPE_F32 else np.uint16
+    q = _c(q, elem)
+    k_cache = _c(k_cache, elem)
+    v_cache = _c(v_cache, elem)
+    B, Nmax, Hq, d = q.shape
+    prefix_len = _c(prefix_len, np.int32)
+    parents = _c(parents, np.int32)
+    n_nodes = _c(n_nodes, np.int32)
+    block_table = _c(block_table, np.int32)
+    if block_table is None:
+        kv_rows = k_cache.shape[2]
+        max_blocks = 0
+    else:
+        kv_rows = k_cache.shape[2]
+        max_blocks = block_table.shape[1]
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    node_mask = _c(node_mask, np.uint8)
+    if out is None:
+        out = np.zeros((B, Nmax, Hq, d), dtype=np.float64)
+    rc = lib.ltd_oracle_tree_verify_attn(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                                         _ptr(prefix_len), _ptr(parents), _ptr(n_nodes),
+                                         _ptr(node_mask), _ptr(out),
+                                         B, Nmax, Hq, Hkv, d, kv_rows, max_blocks, num_blocks,
+                                         float(scale), dtype)
+    if rc != 0:
+        raise OracleError(rc)
+    return out
+
+
+def tree_accept(logits, draft_tokens, parents, n_nodes):
+    """Greedy acceptance.  Returns ``(pred, accepted_nodes, out_tokens, n_accepted)``.
+
+    Entries past ``n_nodes[b]`` (pred) or past ``n_accepted[b]`` (path, tokens)
+    are -1.
+    """
+    lib = _load()
+    logits = _c(logits, np.float32)
+    B, Nmax, Voc = logits.shape
+    draft_tokens = _c(draft_tokens, np.int32)
+    parents = _c(parents, np.int32)
+    n_nodes = _c(n_nodes, np.int32)
+    pred = np.full((B, Nmax), -1, np.int32)
+    acc = np.full((B, Nmax), -1, np.int32)
+    toks = np.full((B, Nmax), -1, np.int32)
+    n_acc = np.zeros((B,), np.int32)
+    rc = lib.ltd_oracle_tree_accept(_ptr(logits), _ptr(draft_tokens), _ptr(parents), _ptr(n_nodes),
+                                    B, Nmax, Voc, _ptr(pred), _ptr(acc), _ptr(toks), _ptr(n_acc))
+    if rc != 0:
+        raise OracleError(rc)
+    return pred, acc, toks, n_acc
+
+
+def kv_compact(k_cache, v_cache, prefix_len, accepted_nodes, n_accepted, *, Hkv, block_table=None,
+               num_blocks=0, num_layers=1, layer_stride_elems=0):
+    """In-place compaction of ``k_cache``/``v_cache`` (numpy, modified).
+
+    ``k_cache``/``v_cache`` hold ``num_layers`` layers ``layer_stride_elems``
+    elements apart; each layer has the single-layer layout.  Returns the new
+    prefix lengths.
+    """
+    lib = _load()
+    assert k_cache.flags["C_CONTIGUOUS"] and v_cache.flags["C_CONTIGUOUS"]
+    assert k_cache.dtype == v_cache.dtype and k_cache.dtype in (np.float32, np.uint16)
+    elem_bytes = k_cache.dtype.itemsize
+    prefix_len = _c(prefix_len, np.int32)
+    accepted_nodes = _c(accepted_nodes, np.int32)
+    n_accepted = _c(n_accepted, np.int32)
+    block_table = _c(block_table, np.int32)
+    B, Nmax = accepted_nodes.shape
+    d = k_cache.shape[-1]
+    kv_rows = k_cache.shape[-2]
+    max_blocks = 0 if block_table is None else block_table.shape[1]
+    new_len = np.zeros((B,), np.int32)
+    rc = lib.ltd_oracle_kv_compact(_ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(prefix_len),
+                                   _ptr(new_len), _ptr(accepted_nodes), _ptr(n_accepted), B, Nmax,
+                                   Hkv, d, kv_rows, max_blocks, num_blocks, num_layers,
+                                   int(layer_stride_elems), elem_bytes)
+    if rc != 0:
+        raise OracleError(rc)
+    return new_len

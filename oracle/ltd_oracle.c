@@ -1,0 +1,336 @@
+/*
+ * CPU oracle for the tree-verification step of Learning-to-Draft speculative
+ * decoding (arXiv 2603.01639).  TEST INFRASTRUCTURE ONLY: loaded by the test
+ * suite, the smoke check and the benchmark's CPU-baseline leg, never by the
+ * GPU library.  It shares no code with the HIP path.
+ *
+ * Every function here writes out the plain definition of the step it stands
+ * for, in fp64, with no blocking, splitting, online softmax or fusion:
+ *
+ *   tree attention   paper section 3.2 ("Candidate Token Selection": the V
+ *                    candidates are flattened into one sequence with a tree
+ *                    attention mask; "Draft Tree Verification": one target pass
+ *                    checks them all in parallel).  The mask lets a candidate
+ *                    see the context prefix and its own ancestors only, so a
+ *                    node's output is ordinary attention of its query over
+ *                    prefix + root path.
+ *   acceptance       paper section 3.2 ("Draft Tree Verification"): tokens are
+ *                    accepted up to the first mismatch with the target's own
+ *                    prediction; the target's prediction at the first error
+ *                    (the bonus token) is appended.
+ *   compaction       the rejected candidates are discarded (same paragraph);
+ *                    the accepted rows are moved next to the prefix.
+ *
+ * Readings of points the paper leaves open (softmax scale, node order, whether
+ * V counts the root, tie rules, where tree K/V live) are fixed by the caller's
+ * arguments or stated at the function that applies them.
+ */
+#include "ltd_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+int ltd_oracle_num_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+/* bf16 is the top half of an IEEE binary32; widening is exact. */
+static double bf16_bits_to_double(uint16_t bits) {
+  uint32_t u = (uint32_t)bits << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+static double load_elem(const void* base, int64_t idx, int dtype) {
+  if (dtype == LTDO_DTYPE_F32) return (double)((const float*)base)[idx];
+  return bf16_bits_to_double(((const uint16_t*)base)[idx]);
+}
+
+/* Element offset of cache row `row` (logical position in sequence b), kv head
+ * g.  Contiguous: [B][Hkv][cap][d].  Paged: [num_blocks][Hkv][block_size][d]
+ * with the physical block taken from block_table[b][row / block_size]. */
+static int64_t cache_row_offset(const int32_t* block_table, int b, int g, int row, int Hkv,
+                                int d, int kv_rows, int max_blocks) {
+  if (block_table == NULL) {
+    return (((int64_t)b * Hkv + g) * kv_rows + row) * (int64_t)d;
+  }
+  int64_t blk = block_table[(int64_t)b * max_blocks + row / kv_rows];
+  return ((blk * Hkv + g) * kv_rows + row % kv_rows) * (int64_t)d;
+}
+
+/* Checks shared by attention: tree shape, prefix bounds and block ids.
+ * Returns 0 or an LTDO_STATUS_* code. */
+static int check_tree_and_cache(const int32_t* block_table, const int32_t* prefix_len,
+                                const int32_t* parents, const int32_t* n_nodes, int B, int Nmax,
+                                int kv_rows, int max_blocks, int num_blocks) {
+  for (int b = 0; b < B; ++b) {
+    int n = n_nodes[b];
+    if (n < 1 || n > Nmax) return LTDO_STATUS_BAD_NNODES;
+    const int32_t* par = parents + (int64_t)b * Nmax;
+    if (par[0] != -1) return LTDO_STATUS_BAD_PARENT;
+    for (int i = 1; i < n; ++i)
+      if (par[i] < 0 || par[i] >= i) return LTDO_STATUS_BAD_PARENT;
+    int P = prefix_len[b];
+    int64_t capacity = block_table ? (int64_t)kv_rows * max_blocks : kv_rows;
+    if (P < 0 || (int64_t)P + n > capacity) return LTDO_STATUS_BAD_PREFIX;
+    if (block_table) {
+      int used = (P + n + kv_rows - 1) / kv_rows;
+      for (int j = 0; j < used; ++j) {
+        int32_t blk = block_table[(int64_t)b * max_blocks + j];
+        if (blk < 0 || blk >= num_blocks) return LTDO_STATUS_BAD_BLOCK;
+      }
+    }
+  }
+  return 0;
+}
+
+int ltd_oracle_tree_verify_attn(const void* q, const void* k_cache, const void* v_cache,
+                                const int32_t* block_table, const int32_t* prefix_len,
+                                const int32_t* parents, const int32_t* n_nodes,
+                                const uint8_t* node_mask, double* out, int B, int Nmax, int Hq,
+                                int Hkv, int d, int kv_rows, int max_blocks, int num_blocks,
+                                double scale, int dtype) {
+  if (!q || !k_cache || !v_cache || !prefix_len || !parents || !n_nodes || !out)
+    return LTDO_EINVAL;
+  if (B < 0 || Nmax < 1 || Hq < 1 || Hkv < 1 || d < 1 || kv_rows < 1 || Hq % Hkv != 0)
+    return LTDO_EINVAL;
+  if (block_table && (max_blocks < 1 || num_blocks < 1)) return LTDO_EINVAL;
+  if (dtype != LTDO_DTYPE_F32 && dtype != LTDO_DTYPE_BF16) return LTDO_EUNSUPPORTED;
+  int st = check_tree_and_cache(block_table, prefix_len, parents, n_nodes, B, Nmax, kv_rows,
+                                max_blocks, num_blocks);
+  if (st) return st;
+
+  const int group = Hq / Hkv; /* GQA: q head h reads kv head h / group */
+  int failed = 0;
+
+#pragma omp parallel
+  {
+    /* Per-thread scratch: the node's root path and one score per visible key. */
+    int max_keys = 0;
+    for (int b = 0; b < B; ++b)
+      if (prefix_len[b] + n_nodes[b] > max_keys) max_keys = prefix_len[b] + n_nodes[b];
+    int* path = (int*)malloc(sizeof(int) * (size_t)Nmax);
+    int* key_rows = (int*)malloc(sizeof(int) * (size_t)(max_keys > 0 ? max_keys : 1));
+    double* score = (double*)malloc(sizeof(double) * (size_t)(max_keys > 0 ? max_keys : 1));
+    double* acc = (double*)malloc(sizeof(double) * (size_t)d);
+    if (!path || !key_rows || !score || !acc) {
+#pragma omp atomic write
+      failed = 1;
+    }
+
+#pragma omp for collapse(2) schedule(dynamic)
+    for (int b = 0; b < B; ++b) {
+      for (int i = 0; i < Nmax; ++i) {
+        if (failed || i >= n_nodes[b]) continue;
+        if (node_mask && !node_mask[(int64_t)b * Nmax + i]) continue;
+        const int P = prefix_len[b];
+        const int32_t* par = parents + (int64_t)b * Nmax;
+
+        /* Visible keys of node i: every prefix row, then the tree rows of its
+         * ancestors (the root path, walked from i up to the root). */
+        int n_keys = 0;
+        for (int t = 0; t < P; ++t) key_rows[n_keys++] = t;
+        int path_len = 0;
+        for (int j = i; j != -1; j = par[j]) path[path_len++] = j;
+        for (int a = 0; a < path_len; ++a) key_rows[n_keys++] = P + path[a];
+
+        for (int h = 0; h < Hq; ++h) {
+          const int g = h / group;
+          const int64_t q_off = (((int64_t)b * Nmax + i) * Hq + h) * d;
+
+          /* s_t = scale * <q, k_t> for every visible key t */
+          double m = -INFINITY;
+          for (int t = 0; t < n_keys; ++t) {
+            int64_t k_off = cache_row_offset(block_table, b, g, key_rows[t], Hkv, d, kv_rows,
+                                             max_blocks);
+            double dot = 0.0;
+            for (int e = 0; e < d; ++e)
+              dot += load_elem(q, q_off + e, dtype) * load_elem(k_cache, k_off + e, dtype);
+            score[t] = scale * dot;
+            if (score[t] > m) m = score[t];
+          }
+
+          /* softmax weights exp(s_t - max) and the weighted sum of V rows */
+          double denom = 0.0;
+          for (int e = 0; e < d; ++e) acc[e] = 0.0;
+          for (int t = 0; t < n_keys; ++t) {
+            double w = exp(score[t] - m);
+            denom += w;
+            int64_t v_off = cache_row_offset(block_table, b, g, key_rows[t], Hkv, d, kv_rows,
+                                             max_blocks);
+            for (int e = 0; e < d; ++e) acc[e] += w * load_elem(v_cache, v_off + e, dtype);
+          }
+          double* o = out + q_off;
+          for (int e = 0; e < d; ++e) o[e] = acc[e] / denom;
+        }
+      }
+    }
+    free(path);
+    free(key_rows);
+    free(score);
+    free(acc);
+  }
+  return failed ? LTDO_EINVAL : 0;
+}
+
+/* argmax over one node's logits; ties go to the lowest vocabulary index.
+ * Plain IEEE comparison, so -0.0 and +0.0 compare equal.  NaN is outside the
+ * contract. */
+static int32_t argmax_row(const float* row, int Voc) {
+  int32_t best = 0;
+  float best_val = row[0];
+  for (int v = 1; v < Voc; ++v) {
+    if (row[v] > best_val) {
+      best_val = row[v];
+      best = v;
+    }
+  }
+  return best;
+}
+
+int ltd_oracle_tree_accept(const float* logits, const int32_t* draft_tokens,
+                           const int32_t* parents, const int32_t* n_nodes, int B, int Nmax,
+                           int Voc, int32_t* pred, int32_t* accepted_nodes,
+                           int32_t* out_tokens, int32_t* n_accepted) {
+  if (!logits || !draft_tokens || !parents || !n_nodes || !pred || !accepted_nodes ||
+      !out_tokens || !n_accepted)
+    return LTDO_EINVAL;
+  if (B < 0 || Nmax < 1 || Voc < 1) return LTDO_EINVAL;
+  for (int b = 0; b < B; ++b) {
+    int n = n_nodes[b];
+    if (n < 1 || n > Nmax) return LTDO_STATUS_BAD_NNODES;
+    const int32_t* par = parents + (int64_t)b * Nmax;
+    if (par[0] != -1) return LTDO_STATUS_BAD_PARENT;
+    for (int i = 1; i < n; ++i)
+      if (par[i] < 0 || par[i] >= i) return LTDO_STATUS_BAD_PARENT;
+  }
+
+  /* 1. The target's own prediction at every node. */
+#pragma omp parallel for collapse(2) schedule(static)
+  for (int b = 0; b < B; ++b)
+    for (int i = 0; i < Nmax; ++i)
+      if (i < n_nodes[b])
+        pred[(int64_t)b * Nmax + i] = argmax_row(logits + ((int64_t)b * Nmax + i) * Voc, Voc);
+
+  for (int b = 0; b < B; ++b) {
+    const int n = n_nodes[b];
+    const int32_t* par = parents + (int64_t)b * Nmax;
+    const int32_t* tok = draft_tokens + (int64_t)b * Nmax;
+    const int32_t* pr = pred + (int64_t)b * Nmax;
+    char* ok = (char*)malloc((size_t)n);
+    int* depth = (int*)malloc(sizeof(int) * (size_t)n);
+    if (!ok || !depth) {
+      free(ok);
+      free(depth);
+      return LTDO_EINVAL;
+    }
+
+    /* 2-3. A draft token is accepted when it equals the target's prediction at
+     * its parent and its parent was accepted; the root (the previous cycle's
+     * bonus token) is always accepted.  parent < child, so index order visits
+     * parents first. */
+    ok[0] = 1;
+    depth[0] = 0;
+    for (int c = 1; c < n; ++c) {
+      ok[c] = ok[par[c]] && (tok[c] == pr[par[c]]);
+      depth[c] = depth[par[c]] + 1;
+    }
+
+    /* 4. The accepted leaf is the deepest accepted node (the longest accepted
+     * root path); among equally deep ones, the smallest node index. */
+    int leaf = 0;
+    for (int c = 1; c < n; ++c)
+      if (ok[c] && depth[c] > depth[leaf]) leaf = c;
+
+    /* 5. The path is the leaf's ancestors, root first. */
+    int len = depth[leaf] + 1;
+    int32_t* path = accepted_nodes + (int64_t)b * Nmax;
+    for (int j = leaf, k = len - 1; j != -1; j = par[j], --k) path[k] = j;
+
+    /* 6. Emitted tokens: the accepted drafts after the root, then the bonus
+     * (the target's prediction at the leaf).  Their count is the acceptance
+     * length L_A, equal to the path length. */
+    int32_t* ot = out_tokens + (int64_t)b * Nmax;
+    for (int k = 1; k < len; ++k) ot[k - 1] = tok[path[k]];
+    ot[len - 1] = pr[leaf];
+    n_accepted[b] = len;
+
+    free(ok);
+    free(depth);
+  }
+  return 0;
+}
+
+int ltd_oracle_kv_compact(void* k_cache, void* v_cache, const int32_t* block_table,
+                          const int32_t* prefix_len, int32_t* new_prefix_len,
+                          const int32_t* accepted_nodes, const int32_t* n_accepted, int B,
+                          int Nmax, int Hkv, int d, int kv_rows, int max_blocks, int num_blocks,
+                          int num_layers, int64_t layer_stride_elems, int elem_bytes) {
+  if (!k_cache || !v_cache || !prefix_len || !new_prefix_len || !accepted_nodes || !n_accepted)
+    return LTDO_EINVAL;
+  if (new_prefix_len == prefix_len) return LTDO_EINVAL;
+  if (B < 0 || Nmax < 1 || Hkv < 1 || d < 1 || kv_rows < 1 || num_layers < 1) return LTDO_EINVAL;
+  if (elem_bytes != 2 && elem_bytes != 4) return LTDO_EUNSUPPORTED;
+  if (block_table && (max_blocks < 1 || num_blocks < 1)) return LTDO_EINVAL;
+
+  int64_t capacity = block_table ? (int64_t)kv_rows * max_blocks : kv_rows;
+  for (int b = 0; b < B; ++b) {
+    int n = n_accepted[b];
+    const int32_t* path = accepted_nodes + (int64_t)b * Nmax;
+    if (n < 1 || n > Nmax) return LTDO_STATUS_BAD_PATH;
+    if (path[0] != 0) return LTDO_STATUS_BAD_PATH;
+    for (int j = 1; j < n; ++j)
+      if (path[j] <= path[j - 1]) return LTDO_STATUS_BAD_PATH;
+    int P = prefix_len[b];
+    if (P < 0 || (int64_t)P + path[n - 1] >= capacity) return LTDO_STATUS_BAD_PREFIX;
+    if (block_table) {
+      int used = (P + path[n - 1] + kv_rows) / kv_rows;
+      for (int j = 0; j < used; ++j) {
+        int32_t blk = block_table[(int64_t)b * max_blocks + j];
+        if (blk < 0 || blk >= num_blocks) return LTDO_STATUS_BAD_BLOCK;
+      }
+    }
+  }
+
+  const size_t row_bytes = (size_t)d * (size_t)elem_bytes;
+  unsigned char* tmp = (unsigned char*)malloc(row_bytes * (size_t)Nmax);
+  if (!tmp) return LTDO_EINVAL;
+  for (int b = 0; b < B; ++b) {
+    const int P = prefix_len[b];
+    const int n = n_accepted[b];
+    const int32_t* path = accepted_nodes + (int64_t)b * Nmax;
+    for (int layer = 0; layer < num_layers; ++layer) {
+      for (int which = 0; which < 2; ++which) {
+        unsigned char* base = (unsigned char*)(which == 0 ? k_cache : v_cache) +
+                              (size_t)(layer * layer_stride_elems) * (size_t)elem_bytes;
+        for (int g = 0; g < Hkv; ++g) {
+          /* Read every accepted row first, then write them back in path
+           * order, so a destination that is also a later source is safe. */
+          for (int j = 0; j < n; ++j) {
+            int64_t off = cache_row_offset(block_table, b, g, P + path[j], Hkv, d, kv_rows,
+                                           max_blocks);
+            memcpy(tmp + (size_t)j * row_bytes, base + (size_t)off * (size_t)elem_bytes,
+                   row_bytes);
+          }
+          for (int j = 0; j < n; ++j) {
+            int64_t off = cache_row_offset(block_table, b, g, P + j, Hkv, d, kv_rows, max_blocks);
+            memcpy(base + (size_t)off * (size_t)elem_bytes, tmp + (size_t)j * row_bytes,
+                   row_bytes);
+          }
+        }
+      }
+    }
+    new_prefix_len[b] = P + n;
+  }
+  free(tmp);
+  return 0;
+}

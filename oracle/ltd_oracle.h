@@ -1,0 +1,76 @@
+/*
+ * CPU oracle for the tree-verification step of Learning-to-Draft speculative
+ * decoding (arXiv 2603.01639).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This library is the slow, plain, fp64 statement of
+ * what the GPU path computes.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load it.  It shares no source, header or
+ * helper with the HIP library, and the HIP library never calls it.
+ *
+ * All pointers are HOST pointers.  Layouts match the HIP library's contract:
+ *   q            [B][Nmax][Hq][d]           f32 or bf16 (stored as uint16 bit patterns)
+ *   k/v cache    contiguous [B][Hkv][cap][d]  (block_table == NULL)
+ *                paged      [num_blocks][Hkv][block_size][d] with
+ *                           block_table [B][max_blocks]
+ *   parents      [B][Nmax]  parents[b][0] = -1, 0 <= parents[b][i] < i
+ *   out          [B][Nmax][Hq][d]  fp64; rows i >= n_nodes[b] are left untouched
+ *   node_mask    [B][Nmax] uint8 or NULL: when given, only nodes with a nonzero
+ *                entry are computed (sampled checks of large workloads)
+ *
+ * Return values: 0 on success, a negative LTDO_E* code for a malformed call,
+ * or a positive LTDO_STATUS_* code for malformed data (nothing is written then).
+ */
+#ifndef LTD_ORACLE_H
+#define LTD_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LTDO_EINVAL (-1)
+#define LTDO_EUNSUPPORTED (-2)
+
+#define LTDO_DTYPE_F32 0
+#define LTDO_DTYPE_BF16 1
+
+#define LTDO_STATUS_BAD_NNODES 1
+#define LTDO_STATUS_BAD_PARENT 2
+#define LTDO_STATUS_BAD_PREFIX 3
+#define LTDO_STATUS_BAD_BLOCK 4
+#define LTDO_STATUS_BAD_PATH 5
+
+/* Tree attention (paper section 3.2: candidates flattened with a tree
+ * attention mask, verified in one target pass).  Node i of sequence b attends
+ * to the prefix rows [0, P_b) and to the tree rows P_b + j for every j on its
+ * own root path; q head h reads kv head h / (Hq / Hkv). */
+int ltd_oracle_tree_verify_attn(const void* q, const void* k_cache, const void* v_cache,
+                                const int32_t* block_table, const int32_t* prefix_len,
+                                const int32_t* parents, const int32_t* n_nodes,
+                                const uint8_t* node_mask, double* out, int B, int Nmax, int Hq,
+                                int Hkv, int d, int kv_rows, int max_blocks, int num_blocks,
+                                double scale, int dtype);
+
+/* Greedy acceptance (paper section 3.2, "Draft Tree Verification"): per-node
+ * target argmax, then the longest root path whose draft tokens all equal the
+ * target prediction at their parent, then the bonus token. */
+int ltd_oracle_tree_accept(const float* logits, const int32_t* draft_tokens,
+                           const int32_t* parents, const int32_t* n_nodes, int B, int Nmax,
+                           int Voc, int32_t* pred, int32_t* accepted_nodes,
+                           int32_t* out_tokens, int32_t* n_accepted);
+
+/* KV compaction: the accepted path's rows move to [P_b, P_b + n_accepted[b]);
+ * new_prefix_len[b] = P_b + n_accepted[b].  elem_bytes is 2 or 4. */
+int ltd_oracle_kv_compact(void* k_cache, void* v_cache, const int32_t* block_table,
+                          const int32_t* prefix_len, int32_t* new_prefix_len,
+                          const int32_t* accepted_nodes, const int32_t* n_accepted, int B,
+                          int Nmax, int Hkv, int d, int kv_rows, int max_blocks, int num_blocks,
+                          int num_layers, int64_t layer_stride_elems, int elem_bytes);
+
+/* Threads the oracle's parallel loops use (OpenMP), for reporting. */
+int ltd_oracle_num_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,362 @@
+"""Seeded synthetic inputs shaped like the paper's verification workloads.
+
+This module only *draws data*: draft trees, tokens, queries, KV caches, target
+logits and paged block tables.  It contains none of the verification step's
+arithmetic (no attention, no argmax, no acceptance walk, no compaction), so the
+GPU path and the CPU oracle can both consume its arrays without sharing any of
+the method's code.
+
+Shapes follow the paper's setting (arXiv 2603.01639): Eagle-style beam trees of
+width W and depth D (section 3.2, "Draft Tree Generation"), a verification size
+V taken as the top-V candidates by cumulative probability (section 3.2,
+"Candidate Token Selection"; the size policy moves V over [20, 240], appendix
+A.2), and Llama-3-8B / Qwen3-32B / 70B-like attention shapes.  The paper's
+datasets and weights are not used: every tensor is synthetic.
+
+Conventions:
+* RNG: ``numpy.random.Generator(PCG64(seed))``; the standard seed of config c,
+  repetition r is ``1639 + 100 * c + r``.
+* bf16 tensors are returned as uint16 bit patterns, rounded to nearest even
+  from the float32 draw.
+* Trees are parent arrays in topological order: ``parents[0] = -1`` and
+  ``0 <= parents[i] < i``.  N counts the root.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import List, Optional
+
+import numpy as np
+
+DTYPE_F32 = 0
+DTYPE_BF16 = 1
+
+
+def rng_for(seed: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def config_seed(config: int, rep: int = 0) -> int:
+    return 1639 + 100 * config + rep
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 to bf16 (nearest, ties to even); return uint16 bits."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32).astype(np.uint64)
+    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return rounded.astype(np.uint16)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+# --------------------------------------------------------------------------- trees
+
+def tree_uniform_parent(rng: np.random.Generator, n: int) -> np.ndarray:
+    """Node i's parent uniform in [0, i-1]; node 0 is the root."""
+    par = np.empty(n, np.int32)
+    par[0] = -1
+    for i in range(1, n):
+        par[i] = rng.integers(0, i)
+    return par
+
+
+def tree_chain(n: int) -> np.ndarray:
+    par = np.arange(-1, n - 1, dtype=np.int32)
+    return par
+
+
+def tree_star(n: int) -> np.ndarray:
+    par = np.zeros(n, np.int32)
+    par[0] = -1
+    return par
+
+
+def tree_random_exact_depth(rng: np.random.Generator, n: int, depth: int) -> np.ndarray:
+    """A chain 0 -> ... -> depth-1 (so the tree has exactly ``depth`` levels),
+    then every further node picks a uniform parent among nodes whose level is
+    below depth-1."""
+    if not (1 <= depth <= n):
+        raise ValueError("need 1 <= depth <= n")
+    par = np.empty(n, np.int32)
+    par[0] = -1
+    level = np.zeros(n, np.int32)
+    for i in range(1, depth):
+        par[i] = i - 1
+        level[i] = i
+    eligible = [i for i in range(depth) if level[i] < depth - 1]
+    for i in range(depth, n):
+        p = eligible[rng.integers(0, len(eligible))]
+        par[i] = p
+        level[i] = level[p] + 1
+        if level[i] < depth - 1:
+            eligible.append(i)
+    return par
+
+
+@dataclasses.dataclass
+class DraftTree:
+    parents: np.ndarray  # int32 [N]
+    tokens: np.ndarray  # int32 [N]; tokens[0] is the root token
+    scores: np.ndarray  # float64 [N] cumulative log-probability (root = 0)
+
+
+def _children_of(parents: np.ndarray) -> List[List[int]]:
+    ch: List[List[int]] = [[] for _ in range(len(parents))]
+    for i in range(1, len(parents)):
+        ch[parents[i]].append(i)
+    return ch
+
+
+def tree_eagle(rng: np.random.Generator, n: int, depth: int, width: int, vocab: int) -> DraftTree:
+    """Beam-like draft tree (section 3.2, "Draft Tree Generation") reranked to
+    the top-``n`` candidates by cumulative score ("Candidate Token Selection").
+
+    ``depth`` counts levels including the root: level 1 is the root's top-W
+    children, then depth-2 rounds each add the W*W children of the current W
+    leaves and keep the top-W of them (by cumulative score) as the next leaves,
+    so the pool has 1 + W + (depth-2) * W^2 nodes.  Conditional log-probs of a
+    node's W children are the logs of the sorted top-W components of a
+    Dirichlet(0.5 * 1_{W+1}) draw; sibling tokens are distinct.  The top-n set
+    is ancestor-closed because scores strictly decrease along a path; the
+    result is re-indexed by (level, score rank).
+    """
+    pool_par = [-1]
+    pool_lvl = [0]
+    pool_score = [0.0]
+    pool_tok = [int(rng.integers(0, vocab))]
+
+    def expand(node: int) -> List[int]:
+        p = np.sort(rng.dirichlet(np.full(width + 1, 0.5)))[::-1][:width]
+        p = np.maximum(p, 1e-300)
+        toks = rng.choice(vocab, size=width, replace=False)
+        out = []
+        for c in range(width):
+            pool_par.append(node)
+            pool_lvl.append(pool_lvl[node] + 1)
+            pool_score.append(pool_score[node] + float(np.log(p[c])))
+            pool_tok.append(int(toks[c]))
+            out.append(len(pool_par) - 1)
+        return out
+
+    if depth >= 2:
+        leaves = expand(0)
+        for _ in range(depth - 2):
+            cand: List[int] = []
+            for leaf in leaves:
+                cand.extend(expand(leaf))
+            cand.sort(key=lambda j: -pool_score[j])
+            leaves = cand[:width]
+    total = len(pool_par)
+    if n > total:
+        raise ValueError(f"tree pool has {total} nodes, asked for {n}")
+    order = sorted(range(total), key=lambda j: -pool_score[j])[:n]
+    keep = set(order)
+    for j in order:  # ancestor closure (guaranteed by strictly decreasing scores)
+        assert pool_par[j] == -1 or pool_par[j] in keep
+    # re-index by (level, score rank)
+    order.sort(key=lambda j: (pool_lvl[j], -pool_score[j]))
+    new_id = {old: new for new, old in enumerate(order)}
+    parents = np.array([-1 if pool_par[j] == -1 else new_id[pool_par[j]] for j in order], np.int32)
+    tokens = np.array([pool_tok[j] for j in order], np.int32)
+    scores = np.array([pool_score[j] for j in order], np.float64)
+    return DraftTree(parents, tokens, scores)
+
+
+def distinct_sibling_tokens(rng: np.random.Generator, parents: np.ndarray, vocab: int) -> np.ndarray:
+    """Uniform tokens with siblings distinct; the root token is uniform too."""
+    n = len(parents)
+    tok = np.empty(n, np.int32)
+    tok[0] = rng.integers(0, vocab)
+    for p, kids in enumerate(_children_of(parents)):
+        if kids:
+            tok[kids] = rng.choice(vocab, size=len(kids), replace=False)
+    return tok
+
+
+def plant_logits(rng: np.random.Generator, logits: np.ndarray, parents: np.ndarray,
+                 tokens: np.ndarray, p_match: float) -> None:
+    """In place: logits[u] ~ N(0,1) gets one entry raised to max(row) + 1.
+
+    For a node with children, with probability ``p_match`` the raised entry is
+    a uniformly chosen child's token (that child is then the target's
+    prediction); otherwise, and for leaves, it is a token no child of u uses.
+    """
+    n, vocab = logits.shape[0], logits.shape[1]
+    kids = _children_of(parents)
+    for u in range(len(parents)):
+        row = logits[u]
+        ch = kids[u]
+        if ch and rng.random() < p_match:
+            t = int(tokens[ch[rng.integers(0, len(ch))]])
+        else:
+            used = set(int(tokens[c]) for c in ch)
+            while True:
+                t = int(rng.integers(0, vocab))
+                if t not in used:
+                    break
+        row[t] = row.max() + np.float32(1.0)
+    del n
+
+
+# --------------------------------------------------------------------------- batches
+
+@dataclasses.dataclass
+class VerifyBatch:
+    """One verification step's inputs (host arrays)."""
+    dtype: int
+    B: int
+    Nmax: int
+    Hq: int
+    Hkv: int
+    d: int
+    Voc: int
+    q: np.ndarray  # [B][Nmax][Hq][d]   f32 or bf16 bits
+    k_cache: np.ndarray  # contiguous [B][Hkv][cap][d] or paged [nblk][Hkv][bs][d]
+    v_cache: np.ndarray
+    prefix_len: np.ndarray  # int32 [B]
+    parents: np.ndarray  # int32 [B][Nmax]
+    n_nodes: np.ndarray  # int32 [B]
+    draft_tokens: np.ndarray  # int32 [B][Nmax]
+    logits: Optional[np.ndarray]  # float32 [B][Nmax][Voc]
+    block_table: Optional[np.ndarray] = None  # int32 [B][max_blocks]
+    block_size: int = 0
+    num_blocks: int = 0
+    label: str = ""
+
+    @property
+    def paged(self) -> bool:
+        return self.block_table is not None
+
+    @property
+    def kv_rows(self) -> int:
+        return self.block_size if self.paged else self.k_cache.shape[2]
+
+    @property
+    def max_blocks(self) -> int:
+        return 0 if self.block_table is None else self.block_table.shape[1]
+
+    @property
+    def max_prefix(self) -> int:
+        return int(self.prefix_len.max()) if self.B else 0
+
+
+def _normal(rng, shape, dtype):
+    x = rng.standard_normal(size=shape, dtype=np.float32)
+    return x if dtype == DTYPE_F32 else f32_to_bf16_bits(x)
+
+
+def make_batch(rng: np.random.Generator, *, dtype: int, Hq: int, Hkv: int, d: int,
+               prefix: List[int], trees: List[np.ndarray], tokens: List[np.ndarray], Voc: int,
+               p_match: Optional[float], Nmax: Optional[int] = None, block_size: int = 0,
+               cap_slack: int = 0, with_logits: bool = True, label: str = "") -> VerifyBatch:
+    """Assemble a batch.  ``p_match=None`` leaves the logits unplanted N(0,1).
+
+    With ``block_size > 0`` the cache is paged: every sequence gets
+    ceil((P_b + N_b) / block_size) blocks whose physical ids are a seeded
+    permutation of the pool; unused block-table entries hold 0.
+    """
+    B = len(prefix)
+    ns = [len(t) for t in trees]
+    Nmax = max(ns) if Nmax is None else Nmax
+    parents = np.full((B, Nmax), -1, np.int32)
+    toks = np.zeros((B, Nmax), np.int32)
+    for b in range(B):
+        parents[b, :ns[b]] = trees[b]
+        toks[b, :ns[b]] = tokens[b]
+    prefix_len = np.array(prefix, np.int32)
+    n_nodes = np.array(ns, np.int32)
+    q = _normal(rng, (B, Nmax, Hq, d), dtype)
+    if block_size > 0:
+        blocks_per = [-(-(prefix[b] + ns[b]) // block_size) for b in range(B)]
+        num_blocks = int(sum(blocks_per))
+        max_blocks = max(blocks_per)
+        perm = rng.permutation(num_blocks).astype(np.int32)
+        table = np.zeros((B, max_blocks), np.int32)
+        pos = 0
+        for b in range(B):
+            table[b, :blocks_per[b]] = perm[pos:pos + blocks_per[b]]
+            pos += blocks_per[b]
+        k = _normal(rng, (num_blocks, Hkv, block_size, d), dtype)
+        v = _normal(rng, (num_blocks, Hkv, block_size, d), dtype)
+    else:
+        table = None
+        num_blocks = 0
+        cap = max(prefix[b] + ns[b] for b in range(B)) + cap_slack
+        k = _normal(rng, (B, Hkv, cap, d), dtype)
+        v = _normal(rng, (B, Hkv, cap, d), dtype)
+    logits = None
+    if with_logits:
+        logits = rng.standard_normal(size=(B, Nmax, Voc), dtype=np.float32)
+        if p_match is not None:
+            for b in range(B):
+                plant_logits(rng, logits[b], trees[b], tokens[b], p_match)
+    return VerifyBatch(dtype=dtype, B=B, Nmax=Nmax, Hq=Hq, Hkv=Hkv, d=d, Voc=Voc, q=q, k_cache=k,
+                       v_cache=v, prefix_len=prefix_len, parents=parents, n_nodes=n_nodes,
+                       draft_tokens=toks, logits=logits, block_table=table, block_size=block_size,
+                       num_blocks=num_blocks, label=label)
+
+
+# --------------------------------------------------------------------------- the five workloads
+
+def config1_tiny_f32(rep: int = 0) -> VerifyBatch:
+    """Tiny fp32: B=1, 8/8 heads, d=64, prefix 128, 16-node uniform-parent
+    tree, vocab 1000, unplanted N(0,1) logits and uniform draft tokens."""
+    rng = rng_for(config_seed(1, rep))
+    par = tree_uniform_parent(rng, 16)
+    tok = rng.integers(0, 1000, size=16).astype(np.int32)
+    return make_batch(rng, dtype=DTYPE_F32, Hq=8, Hkv=8, d=64, prefix=[128], trees=[par],
+                      tokens=[tok], Voc=1000, p_match=None, label="tiny-f32 P128 N16")
+
+
+def config2_8b(rep: int = 0, with_logits: bool = True) -> VerifyBatch:
+    """Llama-3-8B-shaped bf16: 32/8 heads, d=128, prefix 2048, Eagle tree of
+    depth 6 with top-10 expansion reranked to 60 nodes, vocab 128256, p=0.7."""
+    rng = rng_for(config_seed(2, rep))
+    t = tree_eagle(rng, 60, 6, 10, 128256)
+    return make_batch(rng, dtype=DTYPE_BF16, Hq=32, Hkv=8, d=128, prefix=[2048], trees=[t.parents],
+                      tokens=[t.tokens], Voc=128256, p_match=0.7, with_logits=with_logits,
+                      label="8B bf16 P2048 N60")
+
+
+def config3_long(rep: int = 0, with_logits: bool = True) -> VerifyBatch:
+    """As config 2 with prefix 16384 and p=0.8 (long-reasoning context)."""
+    rng = rng_for(config_seed(3, rep))
+    t = tree_eagle(rng, 60, 6, 10, 128256)
+    return make_batch(rng, dtype=DTYPE_BF16, Hq=32, Hkv=8, d=128, prefix=[16384],
+                      trees=[t.parents], tokens=[t.tokens], Voc=128256, p_match=0.8,
+                      with_logits=with_logits, label="8B bf16 P16384 N60")
+
+
+C4_SIZES = (8, 16, 32, 64, 128, 256)
+
+
+def config4_sweep(n: int, depth: int, rep: int = 0, with_logits: bool = True) -> VerifyBatch:
+    """32B-shaped bf16: 64/8 heads, d=128, prefix 4096, random tree with N
+    nodes and exactly ``depth`` levels, vocab 152064, p=0.6."""
+    rng = rng_for(config_seed(4, rep) * 1000 + n * 16 + depth)
+    par = tree_random_exact_depth(rng, n, depth)
+    tok = distinct_sibling_tokens(rng, par, 152064)
+    return make_batch(rng, dtype=DTYPE_BF16, Hq=64, Hkv=8, d=128, prefix=[4096], trees=[par],
+                      tokens=[tok], Voc=152064, p_match=0.6, with_logits=with_logits,
+                      label=f"32B bf16 P4096 N{n} D{depth}")
+
+
+def config5_paged(rep: int = 0, with_logits: bool = True, B: int = 16) -> VerifyBatch:
+    """Batched paged verify: B=16, 70B-shaped 64/8 heads, d=128, prefix
+    uniform in [1024, 8192], 16-token blocks with a shuffled block table, tree
+    size uniform in [16, 128] (Eagle depth-6 trees reranked), vocab 128256,
+    p=0.7."""
+    rng = rng_for(config_seed(5, rep))
+    prefix = [int(rng.integers(1024, 8193)) for _ in range(B)]
+    ns = [int(rng.integers(16, 129)) for _ in range(B)]
+    trees, toks = [], []
+    for b in range(B):
+        t = tree_eagle(rng, ns[b], 6, 10, 128256)
+        trees.append(t.parents)
+        toks.append(t.tokens)
+    return make_batch(rng, dtype=DTYPE_BF16, Hq=64, Hkv=8, d=128, prefix=prefix, trees=trees,
+                      tokens=toks, Voc=128256, p_match=0.7, Nmax=max(ns), block_size=16,
+                      with_logits=with_logits, label="70B bf16 paged B16")

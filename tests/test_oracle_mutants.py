@@ -1,0 +1,115 @@
+"""The oracle's pins are sensitive: plant plausible mistakes in a copy of the
+oracle's C source, build each mutant on the CPU, and check that at least one
+pin fails for every mutant.  (Mistakes are planted in the oracle only.)"""
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+import test_oracle_accept as TA
+import test_oracle_attention as TT
+import test_oracle_compact as TC
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "ltd_oracle.c")
+
+ATTN_PINS = [
+    lambda: TT.test_every_tree_up_to_6_nodes_matches_root_path_attention(4),
+    lambda: TT.test_random_trees_up_to_32_nodes(1),
+    lambda: TT.test_matches_library_sdpa_with_closure_mask(2),
+    lambda: TT.test_single_node_is_decode_attention(),
+    lambda: TT.test_paged_layout_equals_contiguous(),
+]
+ACCEPT_PINS = [
+    lambda: TA.test_worked_examples(),
+    lambda: TA.test_exhaustive_small_trees_all_patterns(5),
+    lambda: TA.test_argmax_ties_and_signed_zero_match_numpy(),
+    lambda: TA.test_greedy_equivalence_on_toy_lm(0),
+]
+COMPACT_PINS = [
+    lambda: TC.test_contiguous_matches_explicit_gather([0, 1, 3, 6]),
+    lambda: TC.test_contiguous_matches_explicit_gather([0, 4, 5, 9, 11]),
+    lambda: TC.test_attention_after_compaction_equals_attention_over_path(),
+    lambda: TC.test_paged_multilayer_bf16_moves_the_same_rows(),
+]
+
+# (name, original text, mutated text, pins expected to notice)
+MUTANTS = [
+    ("tree part dropped (node sees only itself)",
+     "for (int a = 0; a < path_len; ++a) key_rows", "for (int a = 0; a < 1; ++a) key_rows", ATTN_PINS),
+    ("mask uses parent instead of ancestors",
+     "for (int a = 0; a < path_len; ++a) key_rows",
+     "for (int a = 0; a < (path_len < 2 ? path_len : 2); ++a) key_rows", ATTN_PINS),
+    ("last prefix row dropped", "for (int t = 0; t < P; ++t) key_rows",
+     "for (int t = 0; t + 1 < P; ++t) key_rows", ATTN_PINS),
+    ("GQA head mapping interleaved", "const int g = h / group;", "const int g = h % Hkv;", ATTN_PINS),
+    ("scale ignored", "score[t] = scale * dot;", "score[t] = dot;", ATTN_PINS),
+    ("V read at the wrong row", "int64_t v_off = cache_row_offset(block_table, b, g, key_rows[t],",
+     "int64_t v_off = cache_row_offset(block_table, b, g, key_rows[t] ? key_rows[t] - 1 : 0,",
+     ATTN_PINS),
+    ("paged offset ignores the block table",
+     "int64_t blk = block_table[(int64_t)b * max_blocks + row / kv_rows];",
+     "int64_t blk = b * max_blocks + row / kv_rows;", ATTN_PINS),
+    ("parent acceptance not required", "ok[c] = ok[par[c]] && (tok[c] == pr[par[c]]);",
+     "ok[c] = (tok[c] == pr[par[c]]);", ACCEPT_PINS),
+    ("token compared with own prediction", "ok[c] = ok[par[c]] && (tok[c] == pr[par[c]]);",
+     "ok[c] = ok[par[c]] && (tok[c] == pr[c]);", ACCEPT_PINS),
+    ("argmax ties go to the last index", "if (row[v] > best_val) {", "if (row[v] >= best_val) {",
+     ACCEPT_PINS),
+    ("leaf ties go to the largest index", "if (ok[c] && depth[c] > depth[leaf]) leaf = c;",
+     "if (ok[c] && depth[c] >= depth[leaf]) leaf = c;", ACCEPT_PINS),
+    ("bonus taken at the parent", "ot[len - 1] = pr[leaf];",
+     "ot[len - 1] = pr[leaf ? par[leaf] : 0];", ACCEPT_PINS),
+    ("compaction copies row by row in reverse order without staging",
+     "for (int j = 0; j < n; ++j) {\n"
+     "            int64_t off = cache_row_offset(block_table, b, g, P + path[j], Hkv, d, kv_rows,\n"
+     "                                           max_blocks);\n"
+     "            memcpy(tmp + (size_t)j * row_bytes, base + (size_t)off * (size_t)elem_bytes,\n"
+     "                   row_bytes);",
+     "for (int j = n - 1; j >= 0; --j) {\n"
+     "            int64_t off = cache_row_offset(block_table, b, g, P + path[j], Hkv, d, kv_rows,\n"
+     "                                           max_blocks);\n"
+     "            memcpy(tmp + (size_t)j * row_bytes, base + (size_t)off * (size_t)elem_bytes,\n"
+     "                   row_bytes);\n"
+     "            int64_t dst = cache_row_offset(block_table, b, g, P + j, Hkv, d, kv_rows, max_blocks);\n"
+     "            memcpy(base + (size_t)dst * (size_t)elem_bytes, tmp + (size_t)j * row_bytes, row_bytes);",
+     COMPACT_PINS),
+    ("compaction shifts by one row", "int64_t off = cache_row_offset(block_table, b, g, P + j, Hkv",
+     "int64_t off = cache_row_offset(block_table, b, g, P + j + 1, Hkv", COMPACT_PINS),
+]
+
+
+def _build_mutant(tmp_path, idx, orig, mutated):
+    src = open(SRC).read()
+    assert src.count(orig) >= 1, f"mutation anchor not found: {orig!r}"
+    msrc = src.replace(orig, mutated, 1)
+    cpath = tmp_path / f"mutant{idx}.c"
+    cpath.write_text(msrc)
+    so = tmp_path / f"mutant{idx}.so"
+    inc = os.path.dirname(SRC)
+    subprocess.run(["gcc", "-O1", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-I", inc, "-o",
+                    str(so), str(cpath), "-lm"], check=True)
+    return str(so)
+
+
+def _pins_pass(pins):
+    for pin in pins:
+        try:
+            pin()
+        except (AssertionError, oracle.OracleError):
+            return False
+    return True
+
+
+def test_unmutated_oracle_passes_every_pin():
+    assert _pins_pass(ATTN_PINS + ACCEPT_PINS + COMPACT_PINS)
+
+
+@pytest.mark.parametrize("idx", range(len(MUTANTS)), ids=[m[0] for m in MUTANTS])
+def test_every_mutant_is_caught(idx, tmp_path, monkeypatch):
+    name, orig, mutated, pins = MUTANTS[idx]
+    so = _build_mutant(tmp_path, idx, orig, mutated)
+    monkeypatch.setattr(oracle, "_lib", oracle.load_library(so))
+    np.seterr(all="ignore")
+    assert not _pins_pass(pins), f"pins did not notice: {name}"
