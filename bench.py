@@ -1,0 +1,248 @@
+"""Benchmark: one tree-verification step (tree attention + greedy acceptance +
+KV compaction) on one MI355X, on synthetic inputs shaped like the paper's
+Llama-3-8B verification workload.
+
+    python bench.py [--steps K] [--warmup W] [--workload c2|c3|c4|c5] [--no-cpu-baseline]
+
+Prints ONE JSON line.  `value` is microseconds per verify step (lower is
+better), measured with HIP events around K back-to-back steps whose inputs
+are already resident in HBM; the steps rotate over enough copies of the
+inputs (> 2x the 256 MB Infinity Cache) that each step reads cold data.
+`roofline` describes the dominant kernel: algorithmic bytes per launch over
+its average duration, measured with events on the launch stream.
+`cpu_baseline` times the CPU oracle on the host on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, datasheet
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
+METRIC = "µs per tree-verify step + achieved HBM GB/s (% of peak), 1 MI355X"
+MALL_BYTES = 256 << 20
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="c2", choices=["c2", "c3", "c4", "c5"])
+    ap.add_argument("--c4-n", type=int, default=64)
+    ap.add_argument("--c4-depth", type=int, default=6)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="measured HBM traffic per launch (from rocprofv3 counters)")
+    return ap.parse_args()
+
+
+def make_workload(args):
+    from paper_2603_01639_amd import workloads as W
+    if args.workload == "c2":
+        b = W.config2_8b(0)
+        desc = ("Llama-3-8B-shaped bf16 tree verify: batch 1, 32 q / 8 kv heads, head_dim 128, "
+                "prefix 2048, 60-node Eagle tree (depth 6, top-10), vocab 128256, greedy")
+    elif args.workload == "c3":
+        b = W.config3_long(0)
+        desc = ("8B-shaped bf16 long-context tree verify: batch 1, 32 q / 8 kv heads, head_dim 128, "
+                "prefix 16384, 60-node Eagle tree (depth 6), vocab 128256, greedy")
+    elif args.workload == "c4":
+        b = W.config4_sweep(args.c4_n, args.c4_depth)
+        desc = (f"32B-shaped bf16 tree verify: batch 1, 64 q / 8 kv heads, head_dim 128, prefix 4096, "
+                f"random tree N={args.c4_n} depth {args.c4_depth}, vocab 152064, greedy")
+    else:
+        b = W.config5_paged(0)
+        desc = ("70B-shaped bf16 batched paged tree verify: batch 16, 64 q / 8 kv heads, head_dim 128, "
+                "prefix U[1024,8192], 16-token blocks, tree N U[16,128], vocab 128256, greedy")
+    return b, desc
+
+
+def algorithmic_bytes(b):
+    s = 2 if b.dtype == 1 else 4
+    P = b.prefix_len.astype(np.int64)
+    N = b.n_nodes.astype(np.int64)
+    attn = int((P * b.Hkv * b.d * 2 * s).sum() + (N * b.Hkv * b.d * 2 * s).sum()
+               + 2 * (N * b.Hq * b.d * s).sum())
+    accept = int((N * b.Voc * 4).sum())
+    flops = int((4 * b.Hq * N * P * b.d).sum())
+    return attn, accept, flops
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
+              "the verification step is not sharded across GPUs in this build", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2603_01639_amd as ltd
+
+    def to_dev(a):
+        if a is None:
+            return None
+        if a.dtype == np.uint16:  # bf16 bit patterns
+            return torch.from_numpy(a.view(np.int16)).to("cuda").view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+
+    torch.cuda.set_device(0)
+    b, desc = make_workload(args)
+    attn_bytes, accept_bytes, flops = algorithmic_bytes(b)
+    per_copy = b.k_cache.nbytes + b.v_cache.nbytes + b.logits.nbytes + b.q.nbytes
+    copies = max(2, min(32, math.ceil(2.2 * MALL_BYTES / per_copy)))
+
+    # Resident inputs: `copies` independent copies of q/K/V/logits.
+    shared = dict(prefix_len=to_dev(b.prefix_len), parents=to_dev(b.parents),
+                  n_nodes=to_dev(b.n_nodes), tokens=to_dev(b.draft_tokens),
+                  block_table=to_dev(b.block_table))
+    sets = []
+    for _ in range(copies):
+        sets.append(dict(q=to_dev(b.q), k=to_dev(b.k_cache), v=to_dev(b.v_cache),
+                         logits=to_dev(b.logits)))
+    dtype = sets[0]["q"].dtype
+    out = torch.empty(tuple(b.q.shape), dtype=dtype, device="cuda")
+    ws_attn = torch.empty(max(1, ltd.attn_workspace_size(b.B, b.Nmax, b.Hq, b.Hkv, b.d,
+                                                         b.max_prefix, b.dtype)),
+                          dtype=torch.uint8, device="cuda")
+    ws_acc = torch.empty(max(1, ltd.accept_workspace_size(b.B, b.Nmax, b.Voc)), dtype=torch.uint8,
+                         device="cuda")
+    i32 = dict(dtype=torch.int32, device="cuda")
+    pred = torch.empty((b.B, b.Nmax), **i32)
+    acc = torch.empty((b.B, b.Nmax), **i32)
+    toks = torch.empty((b.B, b.Nmax), **i32)
+    nacc = torch.empty((b.B,), **i32)
+    new_len = torch.empty((b.B,), **i32)
+    stream = torch.cuda.current_stream()
+
+    def attn(s):
+        ltd.tree_verify_attn(s["q"], s["k"], s["v"], shared["prefix_len"], shared["parents"],
+                             shared["n_nodes"], out, max_prefix=b.max_prefix,
+                             block_table=shared["block_table"], num_blocks=b.num_blocks,
+                             workspace=ws_attn, stream=stream)
+
+    def accept(s):
+        ltd.tree_accept(s["logits"], shared["tokens"], shared["parents"], shared["n_nodes"], pred,
+                        acc, toks, nacc, workspace=ws_acc, stream=stream)
+
+    def compact(s):
+        ltd.kv_compact(s["k"], s["v"], shared["prefix_len"], new_len, acc, nacc,
+                       block_table=shared["block_table"], num_blocks=b.num_blocks, stream=stream)
+
+    def step(i):
+        s = sets[i % copies]
+        attn(s)
+        accept(s)
+        compact(s)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # ---- timed region: K whole steps back to back
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / args.steps
+
+    # ---- per-call breakdown: events around every call on the launch stream
+    names = ("tree_verify_attn", "tree_accept", "kv_compact")
+    fns = (attn, accept, compact)
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)] for _ in names]
+    for i in range(args.steps):
+        s = sets[i % copies]
+        for k, fn in enumerate(fns):
+            ev[k][i][0].record(stream)
+            fn(s)
+            ev[k][i][1].record(stream)
+    torch.cuda.synchronize()
+    per_call_us = {n: 1e3 * float(np.mean([a.elapsed_time(z) for a, z in ev[k]]))
+                   for k, n in enumerate(names)}
+
+    kernels = {}
+    for n, nbytes in (("tree_verify_attn", attn_bytes), ("tree_accept", accept_bytes)):
+        us = per_call_us[n]
+        gbs = nbytes / (us * 1e-6) / 1e9
+        kernels[n] = {"us": round(us, 3), "alg_bytes": nbytes, "GB/s": round(gbs, 1),
+                      "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+    kernels["tree_verify_attn"]["alg_flops"] = flops
+    kernels["tree_verify_attn"]["TFLOP/s"] = round(
+        flops / (per_call_us["tree_verify_attn"] * 1e-6) / 1e12, 2)
+    kernels["kv_compact"] = {"us": round(per_call_us["kv_compact"], 3)}
+    dom = max(("tree_verify_attn", "tree_accept"), key=lambda n: per_call_us[n])
+    traffic = None
+    if os.path.exists(args.traffic):
+        tr = json.load(open(args.traffic))
+        key = f"{args.workload}:{dom}"
+        if key in tr:
+            traffic = tr[key]
+    roof = {"kernel": dom, "bound": "hbm", "achieved": kernels[dom]["GB/s"], "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": kernels[dom]["hbm_frac"], "traffic": traffic}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(b, args.cpu_seconds)
+
+    rec = {
+        "metric": METRIC,
+        "value": round(ms_per_step * 1e3, 3),
+        "unit": "µs",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if b.dtype == 1 else "f32",
+        "data": "synthetic",
+        "config": {"workload": desc, "batch": b.B, "n_nodes": b.n_nodes.tolist()[:16],
+                   "prefix": b.prefix_len.tolist()[:16], "input_copies_rotated": copies},
+        "roofline": roof,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+def cpu_baseline(b, seconds):
+    """The CPU oracle (fp64 C, OpenMP) on whole verify steps of the same
+    workload, repeated for about `seconds` of wall time."""
+    import oracle
+    reps, t_start = 0, time.perf_counter()
+    while True:
+        oracle.tree_verify_attn(b.q, b.k_cache, b.v_cache, b.prefix_len, b.parents, b.n_nodes,
+                                Hkv=b.Hkv, block_table=b.block_table, num_blocks=b.num_blocks,
+                                dtype=b.dtype)
+        _, acc, _, nacc = oracle.tree_accept(b.logits, b.draft_tokens, b.parents, b.n_nodes)
+        k, v = b.k_cache.copy(), b.v_cache.copy()
+        oracle.kv_compact(k, v, b.prefix_len, acc, nacc, Hkv=b.Hkv, block_table=b.block_table,
+                          num_blocks=b.num_blocks)
+        reps += 1
+        el = time.perf_counter() - t_start
+        if el >= seconds or reps >= 1000:
+            break
+    return {"value": round(el / reps * 1e6, 1), "unit": "µs", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"{reps} whole verify steps of the benchmark workload (attention for every "
+                      f"node and head, acceptance, compaction incl. a cache copy), fp64 C oracle"}
+
+
+if __name__ == "__main__":
+    main()

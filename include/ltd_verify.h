@@ -1,0 +1,173 @@
+/*
+ * ltd_verify: the tree-verification step of Learning-to-Draft speculative
+ * decoding (arXiv 2603.01639, section 3.2) on AMD Instinct MI355X (gfx950).
+ *
+ * One verification step of a draft-and-verify cycle is three calls on one
+ * stream, with no host synchronisation between them:
+ *
+ *   ltd_tree_verify_attn  the target model's attention over its KV-cache prefix
+ *                         plus the N flattened draft-tree candidates, each
+ *                         candidate seeing only the prefix and its own ancestors
+ *                         (the tree attention mask of section 3.2, "Candidate
+ *                         Token Selection" / "Draft Tree Verification");
+ *   ltd_tree_accept       the target's prediction at every node (vocabulary
+ *                         argmax of its logits) and greedy acceptance: the
+ *                         longest root path whose draft tokens all equal the
+ *                         prediction at their parent, plus the target's token at
+ *                         the first mismatch (section 3.2, "Draft Tree
+ *                         Verification");
+ *   ltd_kv_compact        the accepted path's K/V rows move next to the prefix
+ *                         and the rest of the candidates are discarded (same
+ *                         paragraph: the remainder after the first error is
+ *                         dropped).
+ *
+ * Conventions for every call
+ * --------------------------
+ * - All array pointers are DEVICE pointers, owned by the caller.  The library
+ *   never allocates, frees or synchronises; every call is asynchronous on
+ *   `stream` (a hipStream_t passed as void*, NULL = the default stream).
+ * - Return value: LTD_OK, or a negative LTD_E* code when the call itself is
+ *   malformed (nothing is launched then).  These checks use only the scalar
+ *   arguments and pointer nullness.
+ * - Data-dependent checks (tree shape, prefix bounds, block ids, paths) run on
+ *   the device only when `validate != 0`: a validation kernel writes an
+ *   LTD_STATUS_* code to `*status` (0 when the data is well formed) and, when
+ *   it is nonzero, the step's kernels write nothing.  The code reported is the
+ *   one of the lowest failing sequence index, with checks in the order the
+ *   codes are numbered.  With `validate == 0`, malformed data is undefined
+ *   behaviour and `status` may be NULL.
+ * - Trees: N counts the root.  parents[b][0] = -1 and 0 <= parents[b][i] < i
+ *   (a topological order); node 0 is the root (the previous cycle's bonus
+ *   token).  Tree node i of sequence b sits at logical cache row P_b + i.
+ * - Calls on different streams that touch the same buffers race; calls that
+ *   share a workspace must be stream-ordered.
+ */
+#ifndef LTD_VERIFY_H
+#define LTD_VERIFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LTD_OK 0
+#define LTD_EINVAL (-1)       /* null pointer or out-of-range scalar argument */
+#define LTD_EUNSUPPORTED (-2) /* dtype or head_dim the kernels do not implement */
+#define LTD_EWORKSPACE (-3)   /* workspace missing or smaller than the query says */
+#define LTD_EHIP (-4)         /* a HIP runtime call or kernel launch failed */
+
+#define LTD_DTYPE_F32 0  /* IEEE binary32 */
+#define LTD_DTYPE_BF16 1 /* bfloat16 */
+
+#define LTD_STATUS_OK 0
+#define LTD_STATUS_BAD_NNODES 1 /* n_nodes[b] outside [1, Nmax] */
+#define LTD_STATUS_BAD_PARENT 2 /* parents[b][0] != -1 or parents[b][i] outside [0, i) */
+#define LTD_STATUS_BAD_PREFIX 3 /* prefix_len[b] < 0, > max_prefix, or rows past capacity */
+#define LTD_STATUS_BAD_BLOCK 4  /* a block id the sequence uses is outside [0, num_blocks) */
+#define LTD_STATUS_BAD_PATH 5   /* accepted path not 0 = p_0 < p_1 < ..., or n_accepted out of range */
+
+#define LTD_MAX_NODES 256 /* largest Nmax (the paper's size policy spans V in [20, 240]) */
+
+/*
+ * Tree attention (section 3.2: candidates flattened with a tree attention
+ * mask, verified in one target pass).
+ *
+ * For every sequence b, node i < n_nodes[b] and query head h (kv head
+ * g = h / (Hq / Hkv)):
+ *     out[b][i][h] = softmax_t(scale * <q[b][i][h], K[b][g][t]>) . V[b][g][t]
+ * over the visible rows t = {0, ..., P_b - 1} u {P_b + j : j on the root path of
+ * node i, i included}.  Accumulation is fp32; out has the input dtype.
+ *
+ *   q           [B][Nmax][Hq][d] (dtype): the tree nodes' queries (position
+ *               encoding already applied by the caller).
+ *   k_cache,    contiguous (block_table == NULL): [B][Hkv][kv_rows][d], kv_rows
+ *   v_cache     = capacity per sequence;
+ *               paged: [num_blocks][Hkv][kv_rows][d], kv_rows = block size,
+ *               logical row r of sequence b in block block_table[b][r / kv_rows].
+ *               The tree's own K/V rows must already be written at P_b .. P_b+n-1.
+ *   block_table [B][max_blocks] int32 or NULL.
+ *   prefix_len  [B] int32, P_b >= 0.  max_prefix >= every P_b (host bound used
+ *               to size the launch; checked on the device when validate != 0).
+ *   parents     [B][Nmax] int32, n_nodes [B] int32 in [1, Nmax].
+ *   out         [B][Nmax][Hq][d] (dtype); rows i >= n_nodes[b] are not written.
+ *   Hq % Hkv == 0, d in {64, 128}, 1 <= Nmax <= LTD_MAX_NODES.
+ *   scale       softmax scale (1/sqrt(d) for standard attention).
+ *   workspace   device scratch of at least ltd_tree_verify_attn_workspace_size()
+ *               bytes for the same (B, Nmax, Hq, Hkv, d, max_prefix, dtype); its
+ *               contents need no initialisation and are garbage afterwards.
+ */
+size_t ltd_tree_verify_attn_workspace_size(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
+                                           int dtype);
+
+int ltd_tree_verify_attn(const void* q, const void* k_cache, const void* v_cache,
+                         const int32_t* block_table, const int32_t* prefix_len,
+                         const int32_t* parents, const int32_t* n_nodes, void* out, int B, int Nmax,
+                         int Hq, int Hkv, int d, int max_prefix, int kv_rows, int max_blocks,
+                         int num_blocks, float scale, int dtype, void* workspace,
+                         size_t workspace_bytes, int validate, int32_t* status, void* stream);
+
+/*
+ * Greedy acceptance (section 3.2, "Draft Tree Verification").
+ *
+ *   logits        [B][Nmax][Voc] fp32: the target's logits at every node.
+ *   draft_tokens  [B][Nmax] int32; draft_tokens[b][0] is the root token.
+ *   parents, n_nodes as for attention.
+ * Outputs (entries past n_nodes[b] / n_accepted[b] are not written):
+ *   pred           [B][Nmax] int32: argmax_v logits[b][i][v]; ties go to the
+ *                  lowest v and -0.0 equals +0.0 (NaN logits are undefined).
+ *   accepted_nodes [B][Nmax] int32: the accepted root path, root first
+ *                  (accepted_nodes[b][0] = 0).  Node c is accepted when its
+ *                  parent is and draft_tokens[b][c] == pred[b][parent(c)]; the
+ *                  path ends at the deepest accepted node, the smallest index
+ *                  among equally deep ones.
+ *   out_tokens     [B][Nmax] int32: draft tokens of the accepted non-root path
+ *                  nodes, then the bonus token pred[b][leaf].
+ *   n_accepted     [B] int32: path length = number of emitted tokens (L_A).
+ *   workspace      at least ltd_tree_accept_workspace_size(B, Nmax, Voc) bytes.
+ */
+size_t ltd_tree_accept_workspace_size(int B, int Nmax, int Voc);
+
+int ltd_tree_accept(const float* logits, const int32_t* draft_tokens, const int32_t* parents,
+                    const int32_t* n_nodes, int B, int Nmax, int Voc, int32_t* pred,
+                    int32_t* accepted_nodes, int32_t* out_tokens, int32_t* n_accepted,
+                    void* workspace, size_t workspace_bytes, int validate, int32_t* status,
+                    void* stream);
+
+/*
+ * KV compaction (the candidates after the first mismatch are discarded,
+ * section 3.2, "Draft Tree Verification").
+ *
+ * For every sequence b, layer l < num_layers and kv head: logical row
+ * P_b + accepted_nodes[b][j] moves to row P_b + j for j < n_accepted[b], all
+ * reads before the writes they could overlap; then
+ * new_prefix_len[b] = P_b + n_accepted[b].  Rows >= P_b + n_accepted[b] keep
+ * whatever they held.  K and V of layer l start layer_stride_elems elements
+ * after layer l-1; each layer has the attention call's layout.
+ *
+ *   k_cache, v_cache  device caches (modified in place).
+ *   prefix_len        [B] int32 (read); new_prefix_len [B] int32 (written;
+ *                     must not alias prefix_len).
+ *   accepted_nodes    [B][Nmax], n_accepted [B]: as written by ltd_tree_accept.
+ *   d * element size must be a multiple of 16 bytes.
+ */
+int ltd_kv_compact(void* k_cache, void* v_cache, const int32_t* block_table,
+                   const int32_t* prefix_len, int32_t* new_prefix_len,
+                   const int32_t* accepted_nodes, const int32_t* n_accepted, int B, int Nmax,
+                   int Hkv, int d, int kv_rows, int max_blocks, int num_blocks, int num_layers,
+                   int64_t layer_stride_elems, int dtype, int validate, int32_t* status,
+                   void* stream);
+
+/* Number of KV splits the attention launch uses for a sequence with prefix
+ * length `prefix` (introspection for tests and benchmarks; -1 on bad args). */
+int ltd_tree_verify_attn_num_splits(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
+                                    int dtype, int prefix);
+
+/* Library version string. */
+const char* ltd_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LTD_VERIFY_H */

@@ -1,0 +1,188 @@
+"""ltd_verify: the tree-verification step of Learning-to-Draft speculative
+decoding (arXiv 2603.01639, section 3.2) as hand-written HIP kernels for
+MI355X (gfx950), behind the C ABI declared in ``include/ltd_verify.h``.
+
+This module is the thin Python binding: it marshals torch device tensors to
+raw pointers and calls ``libltdverify.so`` through ctypes.  Every step of the
+path runs in the library's kernels; torch only provides device memory and the
+current stream.  There is no fallback: if the library is missing, importing
+the binding's calls raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libltdverify.so")
+
+LTD_OK = 0
+LTD_EINVAL = -1
+LTD_EUNSUPPORTED = -2
+LTD_EWORKSPACE = -3
+LTD_EHIP = -4
+
+DTYPE_F32 = 0
+DTYPE_BF16 = 1
+
+STATUS_OK = 0
+STATUS_BAD_NNODES = 1
+STATUS_BAD_PARENT = 2
+STATUS_BAD_PREFIX = 3
+STATUS_BAD_BLOCK = 4
+STATUS_BAD_PATH = 5
+
+MAX_NODES = 256
+
+EXPORTED = (
+    "ltd_tree_verify_attn_workspace_size",
+    "ltd_tree_verify_attn",
+    "ltd_tree_accept_workspace_size",
+    "ltd_tree_accept",
+    "ltd_kv_compact",
+    "ltd_tree_verify_attn_num_splits",
+    "ltd_version",
+)
+
+
+class LtdError(RuntimeError):
+    def __init__(self, fn, code):
+        super().__init__(f"{fn} returned {code}")
+        self.code = code
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded HIP library.  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python paper_2603_01639_amd/build.py` (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
+        f32 = ctypes.c_float
+        L.ltd_tree_verify_attn_workspace_size.argtypes = [i32] * 7
+        L.ltd_tree_verify_attn_workspace_size.restype = sz
+        L.ltd_tree_verify_attn.argtypes = [P] * 8 + [i32] * 9 + [f32, i32, P, sz, i32, P, P]
+        L.ltd_tree_verify_attn.restype = i32
+        L.ltd_tree_accept_workspace_size.argtypes = [i32] * 3
+        L.ltd_tree_accept_workspace_size.restype = sz
+        L.ltd_tree_accept.argtypes = [P] * 4 + [i32] * 3 + [P] * 5 + [sz, i32, P, P]
+        L.ltd_tree_accept.restype = i32
+        L.ltd_kv_compact.argtypes = [P] * 7 + [i32] * 8 + [i64, i32, i32, P, P]
+        L.ltd_kv_compact.restype = i32
+        L.ltd_tree_verify_attn_num_splits.argtypes = [i32] * 8
+        L.ltd_tree_verify_attn_num_splits.restype = i32
+        L.ltd_version.argtypes = []
+        L.ltd_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _p(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return DTYPE_F32
+    if t.dtype == torch.bfloat16:
+        return DTYPE_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _check(fn, rc):
+    if rc != LTD_OK:
+        raise LtdError(fn, rc)
+
+
+def version() -> str:
+    return lib().ltd_version().decode()
+
+
+def attn_workspace_size(B, Nmax, Hq, Hkv, d, max_prefix, dtype) -> int:
+    return int(lib().ltd_tree_verify_attn_workspace_size(B, Nmax, Hq, Hkv, d, max_prefix, dtype))
+
+
+def attn_num_splits(B, Nmax, Hq, Hkv, d, max_prefix, dtype, prefix) -> int:
+    return int(lib().ltd_tree_verify_attn_num_splits(B, Nmax, Hq, Hkv, d, max_prefix, dtype, prefix))
+
+
+def accept_workspace_size(B, Nmax, Voc) -> int:
+    return int(lib().ltd_tree_accept_workspace_size(B, Nmax, Voc))
+
+
+def _alloc_workspace(nbytes, device):
+    import torch
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def tree_verify_attn(q, k_cache, v_cache, prefix_len, parents, n_nodes, out, *, max_prefix: int,
+                     block_table=None, num_blocks: int = 0, scale: Optional[float] = None,
+                     workspace=None, validate: bool = False, status=None, stream=None):
+    """Tree attention; see ``ltd_tree_verify_attn`` in include/ltd_verify.h.
+
+    Tensors are CUDA (HIP) tensors: q/out ``[B][Nmax][Hq][d]``, caches
+    contiguous ``[B][Hkv][cap][d]`` or paged ``[num_blocks][Hkv][block][d]``.
+    """
+    B, Nmax, Hq, d = q.shape
+    Hkv = k_cache.shape[1]
+    kv_rows = k_cache.shape[2]
+    max_blocks = 0 if block_table is None else block_table.shape[1]
+    dtype = _dtype_code(q)
+    if scale is None:
+        scale = d ** -0.5
+    if workspace is None:
+        workspace = _alloc_workspace(attn_workspace_size(B, Nmax, Hq, Hkv, d, max_prefix, dtype),
+                                     q.device)
+    rc = lib().ltd_tree_verify_attn(
+        _p(q), _p(k_cache), _p(v_cache), _p(block_table), _p(prefix_len), _p(parents), _p(n_nodes),
+        _p(out), B, Nmax, Hq, Hkv, d, int(max_prefix), kv_rows, max_blocks, int(num_blocks),
+        float(scale), dtype, _p(workspace), workspace.numel() * workspace.element_size(),
+        int(validate), _p(status), _stream(stream))
+    _check("ltd_tree_verify_attn", rc)
+    return out
+
+
+def tree_accept(logits, draft_tokens, parents, n_nodes, pred, accepted_nodes, out_tokens,
+                n_accepted, *, workspace=None, validate: bool = False, status=None, stream=None):
+    """Per-node argmax and greedy acceptance; see ``ltd_tree_accept``."""
+    B, Nmax, Voc = logits.shape
+    if workspace is None:
+        workspace = _alloc_workspace(accept_workspace_size(B, Nmax, Voc), logits.device)
+    rc = lib().ltd_tree_accept(
+        _p(logits), _p(draft_tokens), _p(parents), _p(n_nodes), B, Nmax, Voc, _p(pred),
+        _p(accepted_nodes), _p(out_tokens), _p(n_accepted), _p(workspace),
+        workspace.numel() * workspace.element_size(), int(validate), _p(status), _stream(stream))
+    _check("ltd_tree_accept", rc)
+
+
+def kv_compact(k_cache, v_cache, prefix_len, new_prefix_len, accepted_nodes, n_accepted, *,
+               block_table=None, num_blocks: int = 0, num_layers: int = 1,
+               layer_stride_elems: int = 0, validate: bool = False, status=None, stream=None):
+    """In-place KV compaction; see ``ltd_kv_compact``.
+
+    With ``num_layers > 1`` the caches hold the layers ``layer_stride_elems``
+    elements apart and the last three dims are ``[Hkv][rows][d]``.
+    """
+    B, Nmax = accepted_nodes.shape
+    Hkv, kv_rows, d = k_cache.shape[-3], k_cache.shape[-2], k_cache.shape[-1]
+    max_blocks = 0 if block_table is None else block_table.shape[1]
+    rc = lib().ltd_kv_compact(
+        _p(k_cache), _p(v_cache), _p(block_table), _p(prefix_len), _p(new_prefix_len),
+        _p(accepted_nodes), _p(n_accepted), B, Nmax, Hkv, d, kv_rows, max_blocks, int(num_blocks),
+        int(num_layers), int(layer_stride_elems), _dtype_code(k_cache), int(validate), _p(status),
+        _stream(stream))
+    _check("ltd_kv_compact", rc)

@@ -1,0 +1,163 @@
+// The C ABI of ltd_verify (declared in ltd_verify.h): argument checks, launch
+// plans and kernel dispatch.  No allocation, no synchronisation.
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+
+#include "ltd_launch.hpp"
+#include "ltd_verify.h"
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+
+int device_cu_count() {
+  static std::once_flag once[kMaxDevices];
+  static int cus[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  std::call_once(once[dev], [dev] {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      n = 256;
+    cus[dev] = n;
+  });
+  return cus[dev];
+}
+
+bool attn_args_ok(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix, int dtype) {
+  (void)d;
+  (void)dtype;
+  return B >= 0 && Nmax >= 1 && Nmax <= LTD_MAX_NODES && Hq >= 1 && Hkv >= 1 && Hq % Hkv == 0 &&
+         max_prefix >= 0;
+}
+
+bool attn_supported(int d, int dtype) {
+  return (dtype == LTD_DTYPE_F32 || dtype == LTD_DTYPE_BF16) && (d == 64 || d == 128);
+}
+
+ltd::AttnShape make_shape(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix, int kv_rows,
+                          int max_blocks, int dtype) {
+  return ltd::AttnShape{B, Nmax, Hq, Hkv, d, max_prefix, kv_rows, max_blocks, dtype};
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ltd_version(void) { return "ltd_verify 0.1 (gfx950)"; }
+
+size_t ltd_tree_verify_attn_workspace_size(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
+                                           int dtype) {
+  if (!attn_args_ok(B, Nmax, Hq, Hkv, d, max_prefix, dtype) || !attn_supported(d, dtype)) return 0;
+  const ltd::AttnShape s = make_shape(B, Nmax, Hq, Hkv, d, max_prefix, 1, 0, dtype);
+  return ltd::plan_attention(s, device_cu_count()).workspace_bytes;
+}
+
+int ltd_tree_verify_attn_num_splits(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
+                                    int dtype, int prefix) {
+  if (!attn_args_ok(B, Nmax, Hq, Hkv, d, max_prefix, dtype) || !attn_supported(d, dtype) ||
+      prefix < 0 || prefix > max_prefix)
+    return -1;
+  const ltd::AttnShape s = make_shape(B, Nmax, Hq, Hkv, d, max_prefix, 1, 0, dtype);
+  const ltd::AttnPlan p = ltd::plan_attention(s, device_cu_count());
+  if (!p.mfma) return 1;
+  return (prefix + p.split_keys - 1) / p.split_keys + 1;
+}
+
+int ltd_tree_verify_attn(const void* q, const void* k_cache, const void* v_cache,
+                         const int32_t* block_table, const int32_t* prefix_len,
+                         const int32_t* parents, const int32_t* n_nodes, void* out, int B, int Nmax,
+                         int Hq, int Hkv, int d, int max_prefix, int kv_rows, int max_blocks,
+                         int num_blocks, float scale, int dtype, void* workspace,
+                         size_t workspace_bytes, int validate, int32_t* status, void* stream) {
+  if (!attn_args_ok(B, Nmax, Hq, Hkv, d, max_prefix, dtype) || kv_rows < 1) return LTD_EINVAL;
+  if (!attn_supported(d, dtype)) return LTD_EUNSUPPORTED;
+  if (block_table && (max_blocks < 1 || num_blocks < 1)) return LTD_EINVAL;
+  if (validate && !status) return LTD_EINVAL;
+  if (B == 0) return LTD_OK;
+  if (!q || !k_cache || !v_cache || !prefix_len || !parents || !n_nodes || !out) return LTD_EINVAL;
+  const ltd::AttnShape s = make_shape(B, Nmax, Hq, Hkv, d, max_prefix, kv_rows, max_blocks, dtype);
+  const ltd::AttnPlan plan = ltd::plan_attention(s, device_cu_count());
+  if (plan.workspace_bytes > 0 && (!workspace || workspace_bytes < plan.workspace_bytes))
+    return LTD_EWORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (validate) {
+    if (ltd::launch_validate_tree(block_table, prefix_len, parents, n_nodes, B, Nmax, max_prefix,
+                                  kv_rows, max_blocks, num_blocks, true, status, st) != hipSuccess)
+      return LTD_EHIP;
+  }
+  if (ltd::launch_attention(s, plan, q, k_cache, v_cache, block_table, prefix_len, parents,
+                            n_nodes, out, scale, workspace, validate ? status : nullptr,
+                            st) != hipSuccess)
+    return LTD_EHIP;
+  return LTD_OK;
+}
+
+size_t ltd_tree_accept_workspace_size(int B, int Nmax, int Voc) {
+  if (B < 0 || Nmax < 1 || Nmax > LTD_MAX_NODES || Voc < 1) return 0;
+  return ltd::accept_workspace_bytes(B, Nmax, Voc);
+}
+
+int ltd_tree_accept(const float* logits, const int32_t* draft_tokens, const int32_t* parents,
+                    const int32_t* n_nodes, int B, int Nmax, int Voc, int32_t* pred,
+                    int32_t* accepted_nodes, int32_t* out_tokens, int32_t* n_accepted,
+                    void* workspace, size_t workspace_bytes, int validate, int32_t* status,
+                    void* stream) {
+  if (B < 0 || Nmax < 1 || Nmax > LTD_MAX_NODES || Voc < 1) return LTD_EINVAL;
+  if (validate && !status) return LTD_EINVAL;
+  if (B == 0) return LTD_OK;
+  if (!logits || !draft_tokens || !parents || !n_nodes || !pred || !accepted_nodes ||
+      !out_tokens || !n_accepted)
+    return LTD_EINVAL;
+  const size_t need = ltd::accept_workspace_bytes(B, Nmax, Voc);
+  if (!workspace || workspace_bytes < need) return LTD_EWORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (validate) {
+    if (ltd::launch_validate_tree(nullptr, nullptr, parents, n_nodes, B, Nmax, 0, 1, 0, 0, false,
+                                  status, st) != hipSuccess)
+      return LTD_EHIP;
+  }
+  if (ltd::launch_accept(logits, draft_tokens, parents, n_nodes, B, Nmax, Voc, pred,
+                         accepted_nodes, out_tokens, n_accepted, workspace,
+                         validate ? status : nullptr, st) != hipSuccess)
+    return LTD_EHIP;
+  return LTD_OK;
+}
+
+int ltd_kv_compact(void* k_cache, void* v_cache, const int32_t* block_table,
+                   const int32_t* prefix_len, int32_t* new_prefix_len,
+                   const int32_t* accepted_nodes, const int32_t* n_accepted, int B, int Nmax,
+                   int Hkv, int d, int kv_rows, int max_blocks, int num_blocks, int num_layers,
+                   int64_t layer_stride_elems, int dtype, int validate, int32_t* status,
+                   void* stream) {
+  if (B < 0 || Nmax < 1 || Nmax > LTD_MAX_NODES || Hkv < 1 || d < 1 || kv_rows < 1 ||
+      num_layers < 1 || layer_stride_elems < 0)
+    return LTD_EINVAL;
+  if (dtype != LTD_DTYPE_F32 && dtype != LTD_DTYPE_BF16) return LTD_EUNSUPPORTED;
+  const int elem = dtype == LTD_DTYPE_F32 ? 4 : 2;
+  const int row_bytes = d * elem;
+  if (row_bytes % 16 != 0 || row_bytes > 16 * 256) return LTD_EUNSUPPORTED;
+  if (block_table && (max_blocks < 1 || num_blocks < 1)) return LTD_EINVAL;
+  if (validate && !status) return LTD_EINVAL;
+  if (B == 0) return LTD_OK;
+  if (!k_cache || !v_cache || !prefix_len || !new_prefix_len || !accepted_nodes || !n_accepted)
+    return LTD_EINVAL;
+  if (new_prefix_len == prefix_len) return LTD_EINVAL;
+  if (num_layers > 1 && layer_stride_elems == 0) return LTD_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (validate) {
+    if (ltd::launch_validate_path(block_table, prefix_len, accepted_nodes, n_accepted, B, Nmax,
+                                  kv_rows, max_blocks, num_blocks, status, st) != hipSuccess)
+      return LTD_EHIP;
+  }
+  if (ltd::launch_compact(k_cache, v_cache, block_table, prefix_len, new_prefix_len,
+                          accepted_nodes, n_accepted, B, Nmax, Hkv, row_bytes, kv_rows, max_blocks,
+                          num_layers, layer_stride_elems * elem, validate ? status : nullptr,
+                          st) != hipSuccess)
+    return LTD_EHIP;
+  return LTD_OK;
+}
+
+}  // extern "C"

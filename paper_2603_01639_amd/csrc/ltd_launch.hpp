@@ -1,0 +1,55 @@
+// Host-side launchers shared between the kernel sources and the C ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ltd {
+
+// validate.hip
+hipError_t launch_validate_tree(const int32_t* block_table, const int32_t* prefix_len,
+                                const int32_t* parents, const int32_t* n_nodes, int B, int Nmax,
+                                int max_prefix, int kv_rows, int max_blocks, int num_blocks,
+                                bool check_cache, int32_t* status, hipStream_t stream);
+hipError_t launch_validate_path(const int32_t* block_table, const int32_t* prefix_len,
+                                const int32_t* accepted_nodes, const int32_t* n_accepted, int B,
+                                int Nmax, int kv_rows, int max_blocks, int num_blocks,
+                                int32_t* status, hipStream_t stream);
+
+// attn.hip
+struct AttnShape {
+  int B, Nmax, Hq, Hkv, d, max_prefix, kv_rows, max_blocks, dtype;
+};
+struct AttnPlan {
+  int rows;        // stacked query rows per (sequence, kv head) = G * Nmax
+  int row_tiles;   // workgroups along the stacked rows
+  int tile_rows;   // rows per workgroup
+  int split_keys;  // prefix keys per split (multiple of the key tile)
+  int max_splits;  // prefix splits for max_prefix, plus one split for the tree
+  bool mfma;       // bf16 MFMA split-KV path (else the row-wise VALU path)
+  size_t workspace_bytes;
+};
+AttnPlan plan_attention(const AttnShape& s, int num_cus);
+hipError_t launch_attention(const AttnShape& s, const AttnPlan& plan, const void* q,
+                            const void* k_cache, const void* v_cache, const int32_t* block_table,
+                            const int32_t* prefix_len, const int32_t* parents,
+                            const int32_t* n_nodes, void* out, float scale, void* workspace,
+                            const int32_t* status, hipStream_t stream);
+
+// accept.hip
+size_t accept_workspace_bytes(int B, int Nmax, int Voc);
+hipError_t launch_accept(const float* logits, const int32_t* draft_tokens, const int32_t* parents,
+                         const int32_t* n_nodes, int B, int Nmax, int Voc, int32_t* pred,
+                         int32_t* accepted_nodes, int32_t* out_tokens, int32_t* n_accepted,
+                         void* workspace, const int32_t* status, hipStream_t stream);
+
+// compact.hip
+hipError_t launch_compact(void* k_cache, void* v_cache, const int32_t* block_table,
+                          const int32_t* prefix_len, int32_t* new_prefix_len,
+                          const int32_t* accepted_nodes, const int32_t* n_accepted, int B,
+                          int Nmax, int Hkv, int row_bytes, int kv_rows, int max_blocks,
+                          int num_layers, int64_t layer_stride_bytes, const int32_t* status,
+                          hipStream_t stream);
+
+}  // namespace ltd

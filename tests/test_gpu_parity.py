@@ -1,0 +1,147 @@
+"""GPU parity: the HIP library against the CPU oracle on the same seeded
+inputs.  Attention within max-abs 1e-5 (fp32) / 2e-2 (bf16); argmax, accepted
+path, emitted tokens, count and the compacted cache bit-exact."""
+import numpy as np
+import pytest
+
+import gpu_util as U
+from paper_2603_01639_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _full_step(b, node_mask=None):
+    """attention + acceptance + compaction on the GPU vs the oracle."""
+    U.log(f"[parity] {b.label} B={b.B} Nmax={b.Nmax} P={b.prefix_len.tolist()[:4]}")
+    dev = U.upload(b)
+    got = U.gpu_attention(b, dev)
+    want = U.oracle_attention(b, node_mask)
+    err = U.compare_attention(b, got, want, node_mask)
+    U.log(f"[parity] {b.label} attention max-abs {err:.3e}")
+    if b.logits is not None:
+        pred, acc, toks, nacc = U.gpu_accept(b, dev)
+        U.check_accept(b, (pred, acc, toks, nacc))
+        U.check_compact(b, dev, acc, nacc)
+        U.log(f"[parity] {b.label} accept/compact exact, n_accepted={nacc.tolist()[:8]}")
+    return err
+
+
+@pytest.mark.parametrize("rep", range(5))
+def test_config1_tiny_f32(rep):
+    _full_step(W.config1_tiny_f32(rep))
+
+
+@pytest.mark.parametrize("rep", range(5))
+def test_config2_8b_bf16(rep):
+    _full_step(W.config2_8b(rep))
+
+
+@pytest.mark.parametrize("rep", range(2))
+def test_config3_long_prefix(rep):
+    b = W.config3_long(rep)
+    _full_step(b, U.sample_nodes(b, 16, np.random.default_rng(rep)))
+
+
+@pytest.mark.parametrize("n,depth", [(8, 2), (8, 8), (16, 5), (32, 10), (64, 6), (128, 3),
+                                     (128, 10), (256, 10)])
+def test_config4_sweep(n, depth):
+    b = W.config4_sweep(n, depth)
+    _full_step(b, U.sample_nodes(b, 12, np.random.default_rng(n + depth)))
+
+
+def test_config5_paged_batch():
+    b = W.config5_paged()
+    _full_step(b, U.sample_nodes(b, 6, np.random.default_rng(5)))
+
+
+# ----------------------------------------------------------------- edge cases
+
+def _custom(trees, prefix, *, Hq=8, Hkv=2, d=128, dtype=W.DTYPE_BF16, Nmax=None, Voc=3000,
+            block_size=0, seed=0, p_match=0.7, label="custom"):
+    rng = W.rng_for(seed)
+    toks = [W.distinct_sibling_tokens(rng, t, Voc) for t in trees]
+    return W.make_batch(rng, dtype=dtype, Hq=Hq, Hkv=Hkv, d=d, prefix=prefix, trees=trees,
+                        tokens=toks, Voc=Voc, p_match=p_match, Nmax=Nmax, block_size=block_size,
+                        cap_slack=5, label=label)
+
+
+@pytest.mark.parametrize("P", [0, 1, 5, 63, 64, 65, 1000, 2047, 2049])
+def test_ragged_prefix_lengths(P):
+    rng = np.random.default_rng(P)
+    _full_step(_custom([W.tree_uniform_parent(rng, 37)], [P], seed=P, label=f"ragged P={P}"))
+
+
+def test_single_node_tree_is_decode():
+    _full_step(_custom([np.array([-1], np.int32)], [300], label="N=1"))
+
+
+def test_max_nodes_chain_and_star():
+    _full_step(_custom([W.tree_chain(256)], [129], Hq=8, Hkv=8, label="chain N=256"))
+    _full_step(_custom([W.tree_star(256)], [77], Hq=16, Hkv=2, label="star N=256"))
+
+
+def test_padded_rows_untouched_and_mixed_batch():
+    rng = np.random.default_rng(3)
+    trees = [W.tree_uniform_parent(rng, n) for n in (1, 20, 57, 3)]
+    b = _custom(trees, [10, 0, 700, 129], Nmax=64, seed=3, label="mixed batch Nmax=64")
+    dev = U.upload(b)
+    got = U.gpu_attention(b, dev, fill=7.0)
+    filled = U.as_f64(got, b.dtype)
+    for s in range(b.B):
+        assert (filled[s, b.n_nodes[s]:] == 7.0).all()
+    _full_step(b)
+
+
+@pytest.mark.parametrize("dtype,d,G", [(W.DTYPE_F32, 128, 4), (W.DTYPE_F32, 64, 1),
+                                       (W.DTYPE_BF16, 64, 8), (W.DTYPE_BF16, 128, 1)])
+def test_head_dims_dtypes_and_groups(dtype, d, G):
+    rng = np.random.default_rng(d + G)
+    trees = [W.tree_uniform_parent(rng, 45), W.tree_uniform_parent(rng, 12)]
+    _full_step(_custom(trees, [333, 90], Hq=2 * G, Hkv=2, d=d, dtype=dtype, seed=d + G,
+                       label=f"dtype={dtype} d={d} G={G}"))
+
+
+def test_paged_small_blocks_fp32():
+    rng = np.random.default_rng(11)
+    trees = [W.tree_uniform_parent(rng, n) for n in (9, 30, 2)]
+    _full_step(_custom(trees, [40, 100, 3], Hq=4, Hkv=4, d=64, dtype=W.DTYPE_F32, block_size=16,
+                       seed=11, label="paged fp32"))
+
+
+def test_deterministic():
+    b = W.config2_8b(7)
+    U.log(f"[parity] determinism {b.label}")
+    dev = U.upload(b)
+    a1 = U.gpu_attention(b, dev)
+    a2 = U.gpu_attention(b, dev)
+    np.testing.assert_array_equal(a1, a2)
+    r1 = U.gpu_accept(b, dev)
+    r2 = U.gpu_accept(b, dev)
+    for x, y in zip(r1, r2):
+        np.testing.assert_array_equal(x, y)
+
+
+def test_argmax_ties_signed_zero_and_ragged_vocab():
+    """Ties -> lowest index, -0.0 == +0.0, vocab not a multiple of 4 or of the
+    argmax chunk."""
+    for Voc in (5, 1000, 8193, 128257):
+        rng = np.random.default_rng(Voc)
+        n = 6
+        par = W.tree_uniform_parent(rng, n)
+        lg = rng.integers(-3, 3, size=(1, n, Voc)).astype(np.float32)
+        lg[0, 0, :] = -1.0
+        lg[0, 0, Voc // 2] = -0.0
+        lg[0, 0, Voc - 1] = 0.0
+        b = W.VerifyBatch(dtype=W.DTYPE_F32, B=1, Nmax=n, Hq=1, Hkv=1, d=64, Voc=Voc,
+                          q=np.zeros((1, n, 1, 64), np.float32),
+                          k_cache=np.zeros((1, 1, n, 64), np.float32),
+                          v_cache=np.zeros((1, 1, n, 64), np.float32),
+                          prefix_len=np.zeros(1, np.int32), parents=par[None].copy(),
+                          n_nodes=np.array([n], np.int32),
+                          draft_tokens=rng.integers(0, 3, size=(1, n)).astype(np.int32),
+                          logits=lg, label=f"ties Voc={Voc}")
+        U.log(f"[parity] {b.label}")
+        dev = U.upload(b)
+        got = U.gpu_accept(b, dev)
+        want = U.check_accept(b, got)
+        assert want[0][0, 0] == Voc // 2
