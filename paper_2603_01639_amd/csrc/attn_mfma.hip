@@ -1,0 +1,698 @@
+// Split-KV tree attention for bf16 on CDNA4 matrix cores (gfx950), head_dim 128.
+//
+// What is computed (arXiv 2603.01639, section 3.2): the N draft-tree
+// candidates are verified in one pass, each seeing the KV prefix and its own
+// ancestors (the tree attention mask).  For every (sequence b, kv head g) the
+// G = Hq/Hkv query heads of the group and the N tree nodes are stacked into
+// M = G*N query rows (row r = node*G + head-in-group) that share one K/V
+// stream, so both contractions are dense MFMA tiles:
+//
+//   S^T[key][row] = K[key][:] . Q[row][:]        (v_mfma_f32_32x32x16_bf16)
+//   O^T[dim][row] += V^T[dim][key] . P^T[key][row]
+//
+// Work split: grid = (KV split, row tile, b*Hkv + g).  A workgroup of 8
+// wavefronts owns 8*32*QB stacked rows (32*QB per wave) and one KV split: a
+// range of prefix keys or - for the last split - the tree's own N keys under
+// the ancestor mask.  Each split writes an unnormalised partial (running max
+// m, sum l, O) that attn_merge_kernel combines.
+//
+// K/V stream: 64-key tiles move from HBM straight into an LDS ring of
+// kStages slots with global_load_lds_dwordx4 (no register staging); a lane
+// picks the global 16-byte chunk whose LDS position is base + 16*lane, which
+// is how the LDS swizzles are applied.  One barrier per tile.
+//
+// K in LDS: the 32 rows of each 32-key block are stored in the order the
+// S^T operand reads them (row i holds key sigma(i)), with 16-byte chunk c of
+// row i at c ^ (i & 15).  After the MFMA, accumulator register r of lane half
+// h then holds key 16*h + r for the lane's query row, so the scores of one
+// query row sit in one lane, the softmax state and the O^T accumulators are
+// per-lane, and the score registers are directly the P^T operand.
+//
+// V in LDS keeps its natural [key][dim] layout (chunk c of key k at
+// c ^ 4*(k & 3)); the V^T operand comes from ds_read_b64_tr_b16 transpose
+// reads, two per MFMA.
+//
+// The ancestor sets of the tree split are built in LDS as N x 256-bit masks by
+// pointer doubling over the parent links: anc(i) = anc(i) | anc(jump(i)),
+// jump(i) = jump(jump(i)), 8 rounds for N <= 256.
+#include <algorithm>
+
+#include "ltd_device.hpp"
+#include "ltd_launch.hpp"
+
+namespace ltd {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __attribute__((address_space(3))) void lds_void;
+typedef const __attribute__((address_space(1))) void global_cvoid;
+
+constexpr int kD = 128;                        // head dim
+constexpr int kKT = 64;                        // keys per tile
+constexpr int kWaves = 8;                      // waves per workgroup
+constexpr int kThreads = kWaves * kWave;
+constexpr int kAncWords = LTD_MAX_NODES / 32;  // 256 bits per node
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kKBytes = kKT * kD * 2;          // one K tile in LDS (16 KiB)
+constexpr int kVBytes = kKT * kD * 2;          // one V tile in LDS (16 KiB)
+constexpr int kTileBytes = kKBytes + kVBytes;
+constexpr int kLoadsPerTile = 2 * (kKBytes / 16) / kThreads;  // 4 per lane
+constexpr int kKLoads = kLoadsPerTile / 2;  // K (and V) chunks per lane per tile
+// A running max is kept until a score exceeds it by 2^kLazyMax (log2 units):
+// probabilities stay below 2^kLazyMax, exact in fp32 and well inside bf16
+// range, and the O/l rescale runs only when the max really moves.
+constexpr float kLazyMax = 8.f;
+constexpr int kMaxMergeSplits = 1024;          // the merge kernel's weight table (16 KiB)
+#ifndef LTD_WGS_PER_CU
+#define LTD_WGS_PER_CU 1
+#endif
+#ifndef LTD_STAGES
+#define LTD_STAGES 4
+#endif
+#ifndef LTD_QB
+#define LTD_QB 1
+#endif
+constexpr int kWgsPerCu = LTD_WGS_PER_CU;  // resident workgroups the split plan aims for
+constexpr int kStages = LTD_STAGES;        // K/V tiles in the LDS ring
+constexpr int kQB = LTD_QB;                // 32-row MFMA blocks per wave
+constexpr int kTileRows = kWaves * 32 * kQB;
+
+struct MfmaArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* block_table;
+  const int32_t* prefix_len;
+  const int32_t* parents;
+  const int32_t* n_nodes;
+  uint16_t* ws_o;  // [B*Hkv][max_splits][Mpad][128] bf16: the split's O / l
+  float* ws_ml;    // [B*Hkv][max_splits][Mpad][2]: max (log2 units), sum l
+  uint16_t* out;
+  const int32_t* status;
+  int Nmax, Hq, Hkv, G, kv_rows, max_blocks;
+  int Mpad, split_keys, max_splits;
+  float scale_log2;
+};
+
+// A-row i of a 32-key block reads key sigma(i); accumulator register r of lane
+// half h then holds key 16*h + r.
+__device__ __forceinline__ int sigma(int i) {
+  return 16 * ((i >> 2) & 1) + 4 * (i >> 3) + (i & 3);
+}
+__device__ __forceinline__ int swz_v(int key) { return 4 * (key & 3); }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
+}
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ int n_prefix_splits(int P, int split_keys) {
+  return (P + split_keys - 1) / split_keys;
+}
+
+__device__ __forceinline__ lds_void* as_lds(const void* p) { return (lds_void*)(p); }
+__device__ __forceinline__ global_cvoid* as_global(const void* p) { return (global_cvoid*)(p); }
+
+// Transposed 4-key x 16-dim read of a 16-lane group (ds_read_b64_tr_b16):
+// supplier lane s of the group addresses key k0 + s/4, dims d0 + 4*(s%4)..+3;
+// lane p then receives keys k0..k0+3 of dim d0 + p.
+__device__ __forceinline__ s16x4 lds_read_tr(const unsigned char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)as_lds(p));
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Direct global->LDS loads of 16 bytes per lane (global_load_lds_dwordx4;
+// lane i's bytes land at M0 + 16*i).  They are issued as inline assembly on
+// purpose: the compiler does not track them, so it does not put a full
+// vector-memory wait in front of every later LDS read (which would drain the
+// prefetch ring every tile).  The kernel waits for them itself (wait_vmcnt)
+// and orders them across waves with bare barriers.  Nothing else in these
+// kernels uses M0.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(as_lds(p))));
+}
+__device__ __forceinline__ void dma16(uint32_t lds, const void* uniform_base, uint32_t lane_off) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               ::"s"(lds), "v"(lane_off), "s"(uniform_base)
+               : "memory");
+}
+__device__ __forceinline__ void dma16(uint32_t lds, const void* lane_ptr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(lane_ptr)
+               : "memory");
+}
+// Workgroup barrier without the memory fence __syncthreads() adds (that fence
+// would also wait for every outstanding direct load).
+__device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
+
+constexpr int kMaxSplitBlocks = 1024;  // paged block ids one split may span
+constexpr int kMaxSplitKeys = 960;     // <= kMaxSplitBlocks - 2 keys, a multiple of kKT
+
+struct Smem {
+  unsigned char kv[kStages][kTileBytes];
+  uint32_t anc[LTD_MAX_NODES][kAncWords];
+  int16_t jump[2][LTD_MAX_NODES];
+  int32_t blk[kMaxSplitBlocks];  // physical block ids of this split's rows (paged)
+};
+
+// This lane's share of a tile's direct loads: for load u (0..3) the tile row
+// of its K chunk and of its V chunk, the chunk's byte offset within the row,
+// and the wave-uniform LDS byte offset of the wave's 1 KiB destination block.
+struct LoadPlan {
+  int k_key[kKLoads], k_off[kKLoads], v_key[kKLoads], v_off[kKLoads], lds_pos[kKLoads];
+};
+
+__device__ __forceinline__ LoadPlan make_load_plan(int wave, int lane) {
+  LoadPlan lp;
+#pragma unroll
+  for (int u = 0; u < kKLoads; ++u) {
+    const int blk = u * kWaves + wave;    // 1 KiB block = 4 LDS rows of 256 B
+    const int i = blk * 4 + (lane >> 4);  // LDS row
+    const int pc = lane & 15;             // physical 16-byte chunk in the row
+    lp.k_key[u] = (i & 32) + sigma(i & 31);
+    lp.k_off[u] = (pc ^ (i & 15)) * 16;
+    lp.v_key[u] = i;
+    lp.v_off[u] = (pc ^ swz_v(i)) * 16;
+    lp.lds_pos[u] = blk * 1024;
+  }
+  return lp;
+}
+
+// The attention of one workgroup over one KV split.
+template <bool kTree>
+__device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g, int bg, int split,
+                                       int row0, int valid_rows, int key_begin, int n_keys) {
+  const int tid = threadIdx.x;
+  const int wave = tid / kWave;
+  const int lane = tid % kWave;
+  const int h = lane >> 5;
+  const int l32 = lane & 31;
+  const int n = a.n_nodes[b];
+
+  // ---- ancestor masks (tree split): pointer doubling with ring slot 0 as
+  // the second buffer; after 8 rounds the sets are back in sm.anc.
+  if (kTree) {
+    uint32_t* anc_b = reinterpret_cast<uint32_t*>(sm.kv[0]);
+    const int32_t* par = a.parents + static_cast<int64_t>(b) * a.Nmax;
+    for (int i = tid; i < LTD_MAX_NODES; i += kThreads) {
+#pragma unroll
+      for (int w = 0; w < kAncWords; ++w)
+        sm.anc[i][w] = (i < n && (i >> 5) == w) ? (1u << (i & 31)) : 0u;
+      sm.jump[0][i] = static_cast<int16_t>((i > 0 && i < n) ? par[i] : -1);
+    }
+    __syncthreads();
+    // Round r leaves each node's 2^(r+1) nearest ancestors in its set; the
+    // rounds stop once every jump pointer has passed the root (after
+    // ceil(log2(depth + 1)) rounds), and the result is copied back to sm.anc
+    // if it ended in the scratch buffer.
+    uint32_t* cur = &sm.anc[0][0];
+    uint32_t* nxt = anc_b;
+    for (int r = 0; r < 8; ++r) {
+      const int jc = r & 1;
+      int live = 0;
+      for (int i = tid; i < n; i += kThreads) {
+        const int j = sm.jump[jc][i];
+#pragma unroll
+        for (int w = 0; w < kAncWords; ++w)
+          nxt[i * kAncWords + w] = cur[i * kAncWords + w] | (j >= 0 ? cur[j * kAncWords + w] : 0u);
+        const int jj = j >= 0 ? sm.jump[jc][j] : -1;
+        sm.jump[jc ^ 1][i] = static_cast<int16_t>(jj);
+        live |= jj >= 0;
+      }
+      const bool more = __syncthreads_or(live);
+      uint32_t* t = cur;
+      cur = nxt;
+      nxt = t;
+      if (!more) break;
+    }
+    if (cur != &sm.anc[0][0]) {
+      for (int i = tid; i < n * kAncWords; i += kThreads) (&sm.anc[0][0])[i] = cur[i];
+      __syncthreads();
+    }
+  }
+
+  // ---- direct K/V tile loads
+  const LoadPlan lp = make_load_plan(wave, lane);
+  const unsigned char* kbase = reinterpret_cast<const unsigned char*>(a.k);
+  const unsigned char* vbase = reinterpret_cast<const unsigned char*>(a.v);
+  const bool paged = a.block_table != nullptr;
+  const int n_tiles = (n_keys + kKT - 1) / kKT;
+  // Paged caches: this split's block ids are staged in LDS first, so address
+  // generation never waits on a global load.
+  int first_blk = 0;
+  if (paged) {
+    first_blk = key_begin / a.kv_rows;
+    const int n_blk = (key_begin + n_keys - 1) / a.kv_rows - first_blk + 1;
+    const int32_t* bt = a.block_table + static_cast<int64_t>(b) * a.max_blocks + first_blk;
+    for (int j = tid; j < n_blk; j += kThreads) sm.blk[j] = bt[j];
+    __syncthreads();
+  }
+  auto row_byte = [&](int key_in_split) -> int64_t {  // byte offset of a cache row
+    const int row = key_begin + key_in_split;
+    if (!paged) return ((static_cast<int64_t>(b) * a.Hkv + g) * a.kv_rows + row) * (kD * 2);
+    const int64_t blk = sm.blk[row / a.kv_rows - first_blk];
+    return ((blk * a.Hkv + g) * a.kv_rows + row % a.kv_rows) * (kD * 2);
+  };
+  uint32_t k_voff[kKLoads], v_voff[kKLoads];
+#pragma unroll
+  for (int u = 0; u < kKLoads; ++u) {
+    k_voff[u] = static_cast<uint32_t>(lp.k_key[u] * (kD * 2) + lp.k_off[u]);
+    v_voff[u] = static_cast<uint32_t>(lp.v_key[u] * (kD * 2) + lp.v_off[u]);
+  }
+  auto issue_tile = [&](int t) {
+    const unsigned char* k_s = sm.kv[t % kStages];
+    const unsigned char* v_s = k_s + kKBytes;
+    const int tile0 = t * kKT;
+    if (!paged && tile0 + kKT <= n_keys) {
+      // contiguous rows: a uniform tile base plus per-lane 32-bit offsets
+      const int64_t base = row_byte(tile0);
+#pragma unroll
+      for (int u = 0; u < kKLoads; ++u) {
+        dma16(lds_addr(k_s + lp.lds_pos[u]), kbase + base, k_voff[u]);
+        dma16(lds_addr(v_s + lp.lds_pos[u]), vbase + base, v_voff[u]);
+      }
+    } else {
+      // paged rows, or the split's last partial tile (keys past the end read
+      // the last key's row and are masked out)
+#pragma unroll
+      for (int u = 0; u < kKLoads; ++u) {
+        const int kk = min(tile0 + lp.k_key[u], n_keys - 1);
+        const int vk = min(tile0 + lp.v_key[u], n_keys - 1);
+        dma16(lds_addr(k_s + lp.lds_pos[u]), kbase + row_byte(kk) + lp.k_off[u]);
+        dma16(lds_addr(v_s + lp.lds_pos[u]), vbase + row_byte(vk) + lp.v_off[u]);
+      }
+    }
+  };
+
+  // ---- Q fragments (B operand of S^T): lane holds row l32 of each block,
+  // dims 16*kk + 8*h .. +7.
+  bf16x8 qf[kQB][kD / 16];
+  int qnode[kQB];
+#pragma unroll
+  for (int qb = 0; qb < kQB; ++qb) {
+    const int row = row0 + (wave * kQB + qb) * 32 + l32;
+    const bool valid = row < valid_rows;
+    const int node = valid ? row / a.G : 0;
+    const int hg = valid ? row % a.G : 0;
+    qnode[qb] = node;
+    const uint16_t* qrow =
+        a.q + ((static_cast<int64_t>(b) * a.Nmax + node) * a.Hq + g * a.G + hg) * kD;
+#pragma unroll
+    for (int kk = 0; kk < kD / 16; ++kk) {
+      u32x4 v = {0, 0, 0, 0};
+      if (valid) v = *reinterpret_cast<const u32x4*>(qrow + kk * 16 + 8 * h);
+      qf[qb][kk] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+
+  // The Q loads must have landed before the ring starts: the tile loop's
+  // explicit vmcnt waits count only the ring's direct loads.
+#pragma unroll
+  for (int qb = 0; qb < kQB; ++qb)
+#pragma unroll
+    for (int kk = 0; kk < kD / 16; ++kk) asm volatile("" ::"v"(qf[qb][kk]));
+
+#pragma unroll
+  for (int t = 0; t < kStages - 1; ++t)
+    if (t < n_tiles) issue_tile(t);
+
+  // ---- online softmax state (raw score units) and O^T accumulators
+  float m_run[kQB], l_run[kQB];
+  f32x16 o_acc[kQB][kD / 32];
+#pragma unroll
+  for (int qb = 0; qb < kQB; ++qb) {
+    m_run[qb] = -INFINITY;
+    l_run[qb] = 0.f;
+#pragma unroll
+    for (int db = 0; db < kD / 32; ++db) o_acc[qb][db] = f32x16{};
+  }
+  const float c = a.scale_log2;
+
+  // LDS read offsets (bytes within a tile), all loop-invariant:
+  //  K operand, 16-dim step kk: row l32 of the 32-row block, chunk
+  //  (2*kk + h) ^ (l32 & 15).
+  int k_rd[kD / 16];
+#pragma unroll
+  for (int kk = 0; kk < kD / 16; ++kk)
+    k_rd[kk] = l32 * (kD * 2) + (((2 * kk + h) ^ (l32 & 15)) << 4);
+  //  V^T operand: 16-lane group q reads key 16*(q/2) + s/4 (+ the k-step's
+  //  base, a multiple of 4), dims 32*db + 16*(q%2) + 4*(s%4).
+  const int tr_q = lane >> 4, tr_s = lane & 15;
+  const int tr_key = 16 * (tr_q >> 1) + (tr_s >> 2);
+  int v_rd[kD / 32];
+#pragma unroll
+  for (int db = 0; db < kD / 32; ++db) {
+    const int dim = 32 * db + 16 * (tr_q & 1) + 4 * (tr_s & 3);
+    v_rd[db] = tr_key * (kD * 2) + (((dim >> 3) ^ swz_v(tr_key)) << 4) + (dim & 7) * 2;
+  }
+
+  for (int t = 0; t < n_tiles; ++t) {
+    const int ahead = min(kStages - 2, n_tiles - 1 - t);  // tiles in flight behind tile t
+    if (ahead >= 3) wait_vmcnt<3 * kLoadsPerTile>();
+    else if (ahead == 2) wait_vmcnt<2 * kLoadsPerTile>();
+    else if (ahead == 1) wait_vmcnt<kLoadsPerTile>();
+    else wait_vmcnt<0>();
+    barrier_only();  // tile t landed for all waves; every wave is done with tile t-1
+    if (t + kStages - 1 < n_tiles) issue_tile(t + kStages - 1);
+
+    const unsigned char* k_s = sm.kv[t % kStages];
+    const unsigned char* v_s = k_s + kKBytes;
+    const int tile0 = t * kKT;
+
+    // ---- S^T = K Q^T, the two 32-key blocks interleaved
+    f32x16 s_acc[kQB][2];
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb) s_acc[qb][0] = s_acc[qb][1] = f32x16{};
+#pragma unroll
+    for (int k4 = 0; k4 < kD / 64; ++k4) {
+      bf16x8 af[2][4];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          af[kb][u] =
+              *reinterpret_cast<const bf16x8*>(k_s + kb * 32 * (kD * 2) + k_rd[4 * k4 + u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int qb = 0; qb < kQB; ++qb)
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+            s_acc[qb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kb][u], qf[qb][4 * k4 + u],
+                                                                    s_acc[qb][kb], 0, 0, 0);
+    }
+
+    // ---- masks, online softmax, P^T fragments
+    const bool tail = tile0 + kKT > n_keys;
+    bf16x8 pf[kQB][2][2];
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb) {
+      if (kTree || tail) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          const int kfirst = tile0 + kb * 32 + 16 * h;  // key of register r = kfirst + r
+          uint32_t vis = 0xFFFFu;
+          if (kfirst + 16 > n_keys)
+            vis = (kfirst >= n_keys) ? 0u : ((1u << (n_keys - kfirst)) - 1u);
+          if (kTree) vis &= (sm.anc[qnode[qb]][(tile0 + kb * 32) >> 5] >> (16 * h)) & 0xFFFFu;
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (!((vis >> r) & 1u)) s_acc[qb][kb][r] = -INFINITY;
+        }
+      }
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; r += 2)
+          tmax = __builtin_fmaxf(tmax, __builtin_fmaxf(s_acc[qb][kb][r], s_acc[qb][kb][r + 1]));
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
+      // raise the reference max only when a score exceeds it by 2^kLazyMax
+      const float m_new = (tmax * c > m_run[qb] * c + kLazyMax || m_run[qb] == -INFINITY)
+                              ? fmaxf(m_run[qb], tmax)
+                              : m_run[qb];
+      const float neg = (m_new == -INFINITY) ? 0.f : -m_new * c;
+      float psum = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          float p[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            p[j] = exp2_fast(__builtin_fmaf(s_acc[qb][kb][8 * kk + j], c, neg));
+            psum += p[j];
+          }
+          u32x4 pk;
+          pk.x = pack_bf16x2(p[0], p[1]);
+          pk.y = pack_bf16x2(p[2], p[3]);
+          pk.z = pack_bf16x2(p[4], p[5]);
+          pk.w = pack_bf16x2(p[6], p[7]);
+          pf[qb][kb][kk] = __builtin_bit_cast(bf16x8, pk);
+        }
+      }
+      // Rescale only when some lane's reference max moved.
+      if (__builtin_amdgcn_ballot_w64(m_new != m_run[qb]) != 0) {
+        const float alpha = (m_new == -INFINITY) ? 1.f : exp2_fast((m_run[qb] - m_new) * c);
+        l_run[qb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < kD / 32; ++db) o_acc[qb][db] *= alpha;
+      }
+      l_run[qb] += psum;
+      m_run[qb] = m_new;
+    }
+
+    // ---- O^T += V^T P^T; k-step kc = 2*kb + kk covers keys 32*kb + 16*h +
+    // 8*kk .. +7, read as two transposed 4-key reads.
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc) {
+      const int koff = (32 * (kc >> 1) + 8 * (kc & 1)) * (kD * 2);
+      bf16x8 vf[kD / 32];
+#pragma unroll
+      for (int db = 0; db < kD / 32; ++db) {
+        const s16x4 lo = lds_read_tr(v_s + v_rd[db] + koff);
+        const s16x4 hi = lds_read_tr(v_s + v_rd[db] + koff + 4 * (kD * 2));
+        vf[db] =
+            __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+#pragma unroll
+      for (int qb = 0; qb < kQB; ++qb)
+#pragma unroll
+        for (int db = 0; db < kD / 32; ++db)
+          o_acc[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db], pf[qb][kc >> 1][kc & 1],
+                                                                  o_acc[qb][db], 0, 0, 0);
+    }
+  }
+
+  // ---- partial results of this split: (max in log2 units, sum) in fp32 and
+  // the split's normalised output O / l in bf16 (half the bytes of raw fp32
+  // partials; the merge weights each split by 2^(m - M) * l).  The O rows
+  // pass through LDS so that every store writes whole rows: a wave's 32 rows
+  // are one contiguous 8 KiB block of the workspace.
+  constexpr int kRowPitch = kD * 2 + 16;  // padded LDS row (bank spread)
+  static_assert(kWaves * 32 * kQB * kRowPitch <= kStages * kTileBytes, "staging fits the ring");
+  const int64_t part = (static_cast<int64_t>(bg) * a.max_splits + split) * a.Mpad;
+  barrier_only();  // every wave is done with the K/V ring; reuse it for staging
+  unsigned char* stage = &sm.kv[0][0] + wave * (32 * kRowPitch * kQB);  // spans ring slots
+#pragma unroll
+  for (int qb = 0; qb < kQB; ++qb) {
+    const float lsum = l_run[qb] + __shfl_xor(l_run[qb], 32, kWave);
+    const int row = row0 + (wave * kQB + qb) * 32 + l32;
+    if (row < valid_rows && h == 0) {
+      f32x2 ml = {m_run[qb] * c, lsum};
+      *reinterpret_cast<f32x2*>(a.ws_ml + (part + row) * 2) = ml;
+    }
+    const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+    unsigned char* srow = stage + (qb * 32 + l32) * kRowPitch;
+#pragma unroll
+    for (int db = 0; db < kD / 32; ++db) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        uint2 v;
+        v.x = pack_bf16x2(o_acc[qb][db][4 * j] * inv, o_acc[qb][db][4 * j + 1] * inv);
+        v.y = pack_bf16x2(o_acc[qb][db][4 * j + 2] * inv, o_acc[qb][db][4 * j + 3] * inv);
+        *reinterpret_cast<uint2*>(srow + (db * 32 + 8 * j + 4 * h) * 2) = v;
+      }
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  constexpr int kChunks = 32 * kQB * (kD * 2 / 16);  // 16-byte chunks of this wave's rows
+  const int wrow0 = row0 + wave * kQB * 32;
+  unsigned char* gbase = reinterpret_cast<unsigned char*>(a.ws_o + (part + wrow0) * kD);
+#pragma unroll
+  for (int i = 0; i < kChunks / kWave; ++i) {
+    const int cidx = i * kWave + lane;
+    const int r = cidx >> 4, col = cidx & 15;
+    if (wrow0 + r < valid_rows)
+      *reinterpret_cast<u32x4*>(gbase + r * (kD * 2) + col * 16) =
+          *reinterpret_cast<const u32x4*>(stage + r * kRowPitch + col * 16);
+  }
+}
+
+__global__ void __launch_bounds__(kThreads, 1) attn_mfma_kernel(MfmaArgs a) {
+  __shared__ __attribute__((aligned(16))) Smem sm;
+  const int split = blockIdx.x;
+  const int rtile = blockIdx.y;
+  const int bg = blockIdx.z;
+  const int b = bg / a.Hkv;
+  const int g = bg % a.Hkv;
+  if (halted(a.status)) return;
+  const int P = a.prefix_len[b];
+  const int n = a.n_nodes[b];
+  const int nps = n_prefix_splits(P, a.split_keys);
+  if (split > nps) return;
+  const int valid_rows = a.G * n;
+  const int row0 = rtile * kTileRows;
+  if (row0 >= valid_rows) return;
+  if (split == nps)
+    attend<true>(a, sm, b, g, bg, split, row0, valid_rows, P, n);
+  else
+    attend<false>(a, sm, b, g, bg, split, row0, valid_rows, split * a.split_keys,
+                  min(P - split * a.split_keys, a.split_keys));
+}
+
+// One wave per stacked row: combine the splits' partials
+//   out = sum_s w_s * Ohat_s / sum_s w_s,  w_s = 2^(m_s - M) * l_s,  M = max_s m_s,
+// where Ohat_s = O_s / l_s is the split's normalised output (bf16).  Lane s
+// first takes split s's (m, l); then the 4 groups of 16 lanes each read one
+// split's row (16 bytes = 8 dims per lane) per step, so 4 splits' rows are in
+// flight per load, and the groups' sums are added with two lane exchanges.
+__global__ void __launch_bounds__(256) attn_merge_kernel(MfmaArgs a) {
+  __shared__ float w_s[4][kMaxMergeSplits];
+  const int bg = blockIdx.y;
+  const int b = bg / a.Hkv;
+  const int g = bg % a.Hkv;
+  if (halted(a.status)) return;
+  const int wv = threadIdx.x / kWave;
+  const int row = blockIdx.x * 4 + wv;
+  const int lane = threadIdx.x % kWave;
+  const int n = a.n_nodes[b];
+  if (row >= a.G * n) return;
+  // (clamped so that a prefix above the planned maximum cannot index past the
+  // workspace; such input is malformed and caught when validation is on)
+  const int n_splits = min(n_prefix_splits(a.prefix_len[b], a.split_keys) + 1, a.max_splits);
+  const int64_t part0 = static_cast<int64_t>(bg) * a.max_splits * a.Mpad + row;
+  float M = -INFINITY;
+  for (int s = lane; s < n_splits; s += kWave) M = fmaxf(M, a.ws_ml[(part0 + s * a.Mpad) * 2]);
+  M = wave_max(M);
+  float wsum = 0.f;
+  for (int s = lane; s < n_splits; s += kWave) {
+    const f32x2 ml = *reinterpret_cast<const f32x2*>(a.ws_ml + (part0 + s * a.Mpad) * 2);
+    const float w = exp2_fast(ml.x - M) * ml.y;
+    w_s[wv][s] = w;
+    wsum += w;
+  }
+  wsum = wave_sum(wsum);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const int grp = lane >> 4, col = lane & 15;  // split offset, 8-dim chunk
+  const unsigned char* op = reinterpret_cast<const unsigned char*>(a.ws_o + part0 * kD) + col * 16;
+  const int64_t stride = static_cast<int64_t>(a.Mpad) * kD * 2;  // bytes between splits
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < n_splits; s0 += 16) {
+    u32x4 o[4];
+    float w[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int sp = s0 + 4 * u + grp;
+      o[u] = (u32x4){0u, 0u, 0u, 0u};
+      w[u] = 0.f;
+      if (sp < n_splits) {
+        o[u] = *reinterpret_cast<const u32x4*>(op + sp * stride);
+        w[u] = w_s[wv][sp];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[2 * e] += w[u] * bf16_to_f32(static_cast<uint16_t>(o[u][e] & 0xFFFFu));
+        acc[2 * e + 1] += w[u] * bf16_to_f32(static_cast<uint16_t>(o[u][e] >> 16));
+      }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    acc[e] += __shfl_xor(acc[e], 16, kWave);
+    acc[e] += __shfl_xor(acc[e], 32, kWave);
+  }
+  if (grp == 0) {
+    const float inv = 1.f / wsum;
+    const int node = row / a.G;
+    const int hq = g * a.G + row % a.G;
+    uint16_t* orow = a.out + ((static_cast<int64_t>(b) * a.Nmax + node) * a.Hq + hq) * kD;
+    u32x4 v;
+    v.x = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+    v.y = pack_bf16x2(acc[2] * inv, acc[3] * inv);
+    v.z = pack_bf16x2(acc[4] * inv, acc[5] * inv);
+    v.w = pack_bf16x2(acc[6] * inv, acc[7] * inv);
+    *reinterpret_cast<u32x4*>(orow + col * 8) = v;
+  }
+}
+
+}  // namespace
+
+bool mfma_supported(const AttnShape& s) {
+  return s.dtype == LTD_DTYPE_BF16 && s.d == kD &&
+         s.max_prefix <= static_cast<int64_t>(kMaxSplitKeys) * (kMaxMergeSplits - 1);
+}
+
+void plan_mfma(const AttnShape& s, int num_cus, AttnPlan* p) {
+  const int G = s.Hq / s.Hkv;
+  p->rows = G * s.Nmax;
+  p->tile_rows = kTileRows;
+  p->row_tiles = (p->rows + kTileRows - 1) / kTileRows;
+  // Aim for kWgsPerCu resident workgroups per compute unit across the
+  // (sequence, kv head, row tile, split) grid; splits hold at least two tiles
+  // and the merge kernel's table bounds their number.
+  // Workgroups of a (sequence, kv head, row tile) unit: its prefix splits plus
+  // the tree split.  When all units fit one round of resident workgroups, the
+  // split count is chosen so that the whole grid still does: a second, nearly
+  // empty round would double the kernel time.
+  const int64_t units = static_cast<int64_t>(s.B) * s.Hkv * p->row_tiles;
+  const int64_t target = static_cast<int64_t>(kWgsPerCu) * num_cus;
+  const int64_t want = std::max<int64_t>(1, target / units - 1);
+  int sk = static_cast<int>((s.max_prefix + want - 1) / want);
+  sk = std::max(sk, (s.max_prefix + kMaxMergeSplits - 2) / (kMaxMergeSplits - 1));
+  sk = ((sk + kKT - 1) / kKT) * kKT;
+  // At most kMaxSplitKeys keys per split, so that a split's paged block ids
+  // fit the LDS table for any block size.
+  p->split_keys = std::min(std::max(sk, 2 * kKT), kMaxSplitKeys);
+  p->max_splits = (s.max_prefix + p->split_keys - 1) / p->split_keys + 1;
+  const int64_t Mpad = static_cast<int64_t>(p->row_tiles) * kTileRows;
+  const int64_t slots = static_cast<int64_t>(s.B) * s.Hkv * p->max_splits * Mpad;
+  p->workspace_bytes = static_cast<size_t>(slots) * (kD * sizeof(uint16_t) + 2 * sizeof(float));
+  p->mfma = true;
+}
+
+hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q,
+                            const void* k_cache, const void* v_cache, const int32_t* block_table,
+                            const int32_t* prefix_len, const int32_t* parents,
+                            const int32_t* n_nodes, void* out, float scale, void* workspace,
+                            const int32_t* status, hipStream_t stream) {
+  MfmaArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k_cache);
+  a.v = static_cast<const uint16_t*>(v_cache);
+  a.block_table = block_table;
+  a.prefix_len = prefix_len;
+  a.parents = parents;
+  a.n_nodes = n_nodes;
+  const int64_t Mpad = static_cast<int64_t>(p.row_tiles) * kTileRows;
+  const int64_t slots = static_cast<int64_t>(s.B) * s.Hkv * p.max_splits * Mpad;
+  a.ws_o = static_cast<uint16_t*>(workspace);
+  a.ws_ml = reinterpret_cast<float*>(a.ws_o + slots * kD);
+  a.out = static_cast<uint16_t*>(out);
+  a.status = status;
+  a.Nmax = s.Nmax;
+  a.Hq = s.Hq;
+  a.Hkv = s.Hkv;
+  a.G = s.Hq / s.Hkv;
+  a.kv_rows = s.kv_rows;
+  a.max_blocks = s.max_blocks;
+  a.Mpad = static_cast<int>(Mpad);
+  a.split_keys = p.split_keys;
+  a.max_splits = p.max_splits;
+  a.scale_log2 = scale * kLog2e;
+  const dim3 grid(p.max_splits, p.row_tiles, s.B * s.Hkv);
+  hipLaunchKernelGGL(attn_mfma_kernel, grid, dim3(kThreads), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 mgrid(static_cast<unsigned>((Mpad + 3) / 4), s.B * s.Hkv);
+  hipLaunchKernelGGL(attn_merge_kernel, mgrid, dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace ltd

@@ -1,4 +1,5 @@
-// Launch planning and dispatch for tree attention.
+// Launch planning and dispatch for tree attention: bf16 with head_dim 128 runs
+// on the MFMA split-KV kernels, everything else on the row-wise VALU kernel.
 #include "ltd_device.hpp"
 #include "ltd_launch.hpp"
 
@@ -9,10 +10,20 @@ hipError_t launch_attn_rowwise(const AttnShape& s, const void* q, const void* k_
                                const int32_t* prefix_len, const int32_t* parents,
                                const int32_t* n_nodes, void* out, float scale,
                                const int32_t* status, hipStream_t stream);
+bool mfma_supported(const AttnShape& s);
+void plan_mfma(const AttnShape& s, int num_cus, AttnPlan* p);
+hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q,
+                            const void* k_cache, const void* v_cache, const int32_t* block_table,
+                            const int32_t* prefix_len, const int32_t* parents,
+                            const int32_t* n_nodes, void* out, float scale, void* workspace,
+                            const int32_t* status, hipStream_t stream);
 
 AttnPlan plan_attention(const AttnShape& s, int num_cus) {
-  (void)num_cus;
   AttnPlan p{};
+  if (mfma_supported(s)) {
+    plan_mfma(s, num_cus, &p);
+    return p;
+  }
   p.rows = (s.Hq / s.Hkv) * s.Nmax;
   p.row_tiles = 1;
   p.tile_rows = p.rows;
@@ -28,8 +39,9 @@ hipError_t launch_attention(const AttnShape& s, const AttnPlan& plan, const void
                             const int32_t* prefix_len, const int32_t* parents,
                             const int32_t* n_nodes, void* out, float scale, void* workspace,
                             const int32_t* status, hipStream_t stream) {
-  (void)plan;
-  (void)workspace;
+  if (plan.mfma)
+    return launch_attn_mfma(s, plan, q, k_cache, v_cache, block_table, prefix_len, parents,
+                            n_nodes, out, scale, workspace, status, stream);
   return launch_attn_rowwise(s, q, k_cache, v_cache, block_table, prefix_len, parents, n_nodes,
                              out, scale, status, stream);
 }
