@@ -142,9 +142,17 @@ __device__ __forceinline__ void wait_vmcnt() {
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(as_lds(p))));
 }
+// Base pointer that the compiler must keep in scalar registers (the SADDR
+// form of the load takes a 64-bit SGPR pair).
+__device__ __forceinline__ const void* scalar_ptr(const void* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+  return reinterpret_cast<const void*>((static_cast<uint64_t>(hi) << 32) | lo);
+}
 __device__ __forceinline__ void dma16(uint32_t lds, const void* uniform_base, uint32_t lane_off) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
-               ::"s"(lds), "v"(lane_off), "s"(uniform_base)
+               ::"s"(lds), "v"(lane_off), "s"(scalar_ptr(uniform_base))
                : "memory");
 }
 __device__ __forceinline__ void dma16(uint32_t lds, const void* lane_ptr) {
@@ -161,6 +169,7 @@ constexpr int kMaxSplitKeys = 960;     // <= kMaxSplitBlocks - 2 keys, a multipl
 struct Smem {
   unsigned char kv[kStages][kTileBytes];
   uint32_t anc[LTD_MAX_NODES][kAncWords];
+  uint32_t anc_tmp[LTD_MAX_NODES][kAncWords];  // second buffer of the mask build
   int16_t jump[2][LTD_MAX_NODES];
   int32_t blk[kMaxSplitBlocks];  // physical block ids of this split's rows (paged)
 };
@@ -198,48 +207,6 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   const int h = lane >> 5;
   const int l32 = lane & 31;
   const int n = a.n_nodes[b];
-
-  // ---- ancestor masks (tree split): pointer doubling with ring slot 0 as
-  // the second buffer; after 8 rounds the sets are back in sm.anc.
-  if (kTree) {
-    uint32_t* anc_b = reinterpret_cast<uint32_t*>(sm.kv[0]);
-    const int32_t* par = a.parents + static_cast<int64_t>(b) * a.Nmax;
-    for (int i = tid; i < LTD_MAX_NODES; i += kThreads) {
-#pragma unroll
-      for (int w = 0; w < kAncWords; ++w)
-        sm.anc[i][w] = (i < n && (i >> 5) == w) ? (1u << (i & 31)) : 0u;
-      sm.jump[0][i] = static_cast<int16_t>((i > 0 && i < n) ? par[i] : -1);
-    }
-    __syncthreads();
-    // Round r leaves each node's 2^(r+1) nearest ancestors in its set; the
-    // rounds stop once every jump pointer has passed the root (after
-    // ceil(log2(depth + 1)) rounds), and the result is copied back to sm.anc
-    // if it ended in the scratch buffer.
-    uint32_t* cur = &sm.anc[0][0];
-    uint32_t* nxt = anc_b;
-    for (int r = 0; r < 8; ++r) {
-      const int jc = r & 1;
-      int live = 0;
-      for (int i = tid; i < n; i += kThreads) {
-        const int j = sm.jump[jc][i];
-#pragma unroll
-        for (int w = 0; w < kAncWords; ++w)
-          nxt[i * kAncWords + w] = cur[i * kAncWords + w] | (j >= 0 ? cur[j * kAncWords + w] : 0u);
-        const int jj = j >= 0 ? sm.jump[jc][j] : -1;
-        sm.jump[jc ^ 1][i] = static_cast<int16_t>(jj);
-        live |= jj >= 0;
-      }
-      const bool more = __syncthreads_or(live);
-      uint32_t* t = cur;
-      cur = nxt;
-      nxt = t;
-      if (!more) break;
-    }
-    if (cur != &sm.anc[0][0]) {
-      for (int i = tid; i < n * kAncWords; i += kThreads) (&sm.anc[0][0])[i] = cur[i];
-      __syncthreads();
-    }
-  }
 
   // ---- direct K/V tile loads
   const LoadPlan lp = make_load_plan(wave, lane);
@@ -294,6 +261,11 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     }
   };
 
+  // First tiles in flight before anything else is loaded.
+#pragma unroll
+  for (int t = 0; t < kStages - 1; ++t)
+    if (t < n_tiles) issue_tile(t);
+
   // ---- Q fragments (B operand of S^T): lane holds row l32 of each block,
   // dims 16*kk + 8*h .. +7.
   bf16x8 qf[kQB][kD / 16];
@@ -315,16 +287,71 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     }
   }
 
-  // The Q loads must have landed before the ring starts: the tile loop's
-  // explicit vmcnt waits count only the ring's direct loads.
+  // The tree's parent links, for wave 0 (lane l handles nodes l + 64*k).
+  constexpr int kNodesPerLane = LTD_MAX_NODES / kWave;
+  int my_parent[kNodesPerLane];
+#pragma unroll
+  for (int k = 0; k < kNodesPerLane; ++k) {
+    const int i = lane + kWave * k;
+    my_parent[k] = -1;
+    if (kTree && wave == 0 && i > 0 && i < n)
+      my_parent[k] = a.parents[static_cast<int64_t>(b) * a.Nmax + i];
+  }
+
+  // The Q loads (and the tree's parent links) must have landed before the
+  // tile loop: its explicit vmcnt waits count only the ring's direct loads.
+  // Waiting here also lets the first tiles, issued before Q, arrive.
 #pragma unroll
   for (int qb = 0; qb < kQB; ++qb)
 #pragma unroll
     for (int kk = 0; kk < kD / 16; ++kk) asm volatile("" ::"v"(qf[qb][kk]));
-
 #pragma unroll
-  for (int t = 0; t < kStages - 1; ++t)
-    if (t < n_tiles) issue_tile(t);
+  for (int k = 0; k < kNodesPerLane; ++k) asm volatile("" ::"v"(my_parent[k]));
+
+  // ---- ancestor masks (tree split): wave 0 builds them by pointer doubling,
+  // anc(i) |= anc(jump(i)), jump(i) = jump(jump(i)), with wave-level ordering
+  // only; it stops once every jump pointer has passed the root (after
+  // ceil(log2(depth + 1)) rounds).  The other waves go on to the tile loop,
+  // whose first barrier publishes the masks.
+  if (kTree && wave == 0) {
+    uint32_t* cur = &sm.anc[0][0];
+    uint32_t* nxt = &sm.anc_tmp[0][0];
+#pragma unroll
+    for (int k = 0; k < kNodesPerLane; ++k) {
+      const int i = lane + kWave * k;
+#pragma unroll
+      for (int w = 0; w < kAncWords; ++w)
+        cur[i * kAncWords + w] = (i < n && (i >> 5) == w) ? (1u << (i & 31)) : 0u;
+      sm.jump[0][i] = static_cast<int16_t>(my_parent[k]);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    for (int r = 0; r < 8; ++r) {
+      const int jc = r & 1;
+      bool live = false;
+#pragma unroll
+      for (int k = 0; k < kNodesPerLane; ++k) {
+        const int i = lane + kWave * k;
+        if (i < n) {
+          const int j = sm.jump[jc][i];
+#pragma unroll
+          for (int w = 0; w < kAncWords; ++w)
+            nxt[i * kAncWords + w] = cur[i * kAncWords + w] | (j >= 0 ? cur[j * kAncWords + w] : 0u);
+          const int jj = j >= 0 ? sm.jump[jc][j] : -1;
+          sm.jump[jc ^ 1][i] = static_cast<int16_t>(jj);
+          live |= jj >= 0;
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      uint32_t* t = cur;
+      cur = nxt;
+      nxt = t;
+      if (__builtin_amdgcn_ballot_w64(live) == 0) break;
+    }
+    if (cur != &sm.anc[0][0]) {
+      for (int i = lane; i < n * kAncWords; i += kWave) (&sm.anc[0][0])[i] = cur[i];
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  }
 
   // ---- online softmax state (raw score units) and O^T accumulators
   float m_run[kQB], l_run[kQB];
