@@ -30,6 +30,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, datasheet
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
 METRIC = "µs per tree-verify step + achieved HBM GB/s (% of peak), 1 MI355X"
 MALL_BYTES = 256 << 20
+CALIB_BYTES = 256 << 20  # device copy used to calibrate HBM byte counters
 
 
 def parse():
@@ -42,8 +43,8 @@ def parse():
     ap.add_argument("--c4-depth", type=int, default=6)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
-                    help="measured HBM traffic per launch (from rocprofv3 counters)")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic.txt"),
+                    help="measured HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE summary)")
     return ap.parse_args()
 
 
@@ -145,6 +146,13 @@ def main():
         accept(s)
         compact(s)
 
+    # A plain device copy of known size, outside the timed region: under
+    # rocprofv3 counter collection it calibrates FETCH_SIZE / WRITE_SIZE.
+    calib = torch.empty(CALIB_BYTES, dtype=torch.uint8, device="cuda")
+    calib2 = torch.empty_like(calib)
+    calib2.copy_(calib)
+    del calib, calib2
+
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
@@ -186,12 +194,7 @@ def main():
         flops / (per_call_us["tree_verify_attn"] * 1e-6) / 1e12, 2)
     kernels["kv_compact"] = {"us": round(per_call_us["kv_compact"], 3)}
     dom = max(("tree_verify_attn", "tree_accept"), key=lambda n: per_call_us[n])
-    traffic = None
-    if os.path.exists(args.traffic):
-        tr = json.load(open(args.traffic))
-        key = f"{args.workload}:{dom}"
-        if key in tr:
-            traffic = tr[key]
+    traffic = read_traffic(args.traffic, args.workload, dom)
     roof = {"kernel": dom, "bound": "hbm", "achieved": kernels[dom]["GB/s"], "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": kernels[dom]["hbm_frac"], "traffic": traffic}
 
@@ -219,6 +222,26 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
+
+
+def read_traffic(path, workload, call):
+    """HBM bytes per launch of `call` from the counter summary: a line
+    `traffic <workload> <call> <bytes> <source hash>` whose hash still matches
+    the attention/accept sources (otherwise the kernel changed: null)."""
+    if not os.path.exists(path):
+        return None
+    import hashlib
+    src = os.path.join(ROOT, "paper_2603_01639_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(src)):
+        if f.endswith((".hip", ".hpp")):
+            h.update(open(os.path.join(src, f), "rb").read())
+    digest = h.hexdigest()[:16]
+    for line in open(path):
+        parts = line.split()
+        if len(parts) == 5 and parts[0] == "traffic" and parts[1] == workload and parts[2] == call:
+            return int(parts[3]) if parts[4] == digest else None
+    return None
 
 
 def cpu_baseline(b, seconds):

@@ -60,3 +60,14 @@ def test_binding_signatures_match_header():
     assert set(protos) == set(ltd.EXPORTED)
     for name, nparams in protos.items():
         assert len(getattr(lib, name).argtypes) == nparams, name
+
+
+def test_bf16_head128_workloads_plan_the_mfma_split_path():
+    """The 8B/32B/70B-shaped bf16 shapes run on the MFMA split-KV kernels
+    (more than one split and a workspace), fp32 and d=64 on the row-wise one."""
+    for B, Nmax, Hq, Hkv, P in ((1, 60, 32, 8, 2048), (1, 60, 32, 8, 16384), (1, 256, 64, 8, 4096),
+                                (16, 128, 64, 8, 8192)):
+        assert ltd.attn_num_splits(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16, P) > 1
+        assert ltd.attn_workspace_size(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16) > 0
+    assert ltd.attn_num_splits(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32, 128) == 1
+    assert ltd.attn_workspace_size(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32) == 0
