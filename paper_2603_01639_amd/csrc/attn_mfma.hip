@@ -76,13 +76,9 @@ constexpr int kMaxMergeSplits = 1024;          // the merge kernel's weight tabl
 #ifndef LTD_STAGES
 #define LTD_STAGES 4
 #endif
-#ifndef LTD_QB
-#define LTD_QB 1
-#endif
 constexpr int kWgsPerCu = LTD_WGS_PER_CU;  // resident workgroups the split plan aims for
 constexpr int kStages = LTD_STAGES;        // K/V tiles in the LDS ring
-constexpr int kQB = LTD_QB;                // 32-row MFMA blocks per wave
-constexpr int kTileRows = kWaves * 32 * kQB;
+constexpr int kTileRows = kWaves * 32;       // stacked query rows per workgroup
 
 struct MfmaArgs {
   const uint16_t* q;
@@ -263,27 +259,24 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
 
   // First tiles in flight before anything else is loaded.
 #pragma unroll
-  for (int t = 0; t < kStages - 1; ++t)
+  for (int t = 0; t < kStages - 2; ++t)
     if (t < n_tiles) issue_tile(t);
 
-  // ---- Q fragments (B operand of S^T): lane holds row l32 of each block,
-  // dims 16*kk + 8*h .. +7.
-  bf16x8 qf[kQB][kD / 16];
-  int qnode[kQB];
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
-    const int row = row0 + (wave * kQB + qb) * 32 + l32;
-    const bool valid = row < valid_rows;
-    const int node = valid ? row / a.G : 0;
-    const int hg = valid ? row % a.G : 0;
-    qnode[qb] = node;
+  // ---- Q fragment (B operand of S^T): lane holds row l32 of the wave's
+  // 32-row block, dims 16*kk + 8*h .. +7.
+  bf16x8 qf[kD / 16];
+  const int qrow_idx = row0 + wave * 32 + l32;
+  const bool qvalid = qrow_idx < valid_rows;
+  const int qnode = qvalid ? qrow_idx / a.G : 0;
+  {
+    const int hg = qvalid ? qrow_idx % a.G : 0;
     const uint16_t* qrow =
-        a.q + ((static_cast<int64_t>(b) * a.Nmax + node) * a.Hq + g * a.G + hg) * kD;
+        a.q + ((static_cast<int64_t>(b) * a.Nmax + qnode) * a.Hq + g * a.G + hg) * kD;
 #pragma unroll
     for (int kk = 0; kk < kD / 16; ++kk) {
       u32x4 v = {0, 0, 0, 0};
-      if (valid) v = *reinterpret_cast<const u32x4*>(qrow + kk * 16 + 8 * h);
-      qf[qb][kk] = __builtin_bit_cast(bf16x8, v);
+      if (qvalid) v = *reinterpret_cast<const u32x4*>(qrow + kk * 16 + 8 * h);
+      qf[kk] = __builtin_bit_cast(bf16x8, v);
     }
   }
 
@@ -302,9 +295,7 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   // tile loop: its explicit vmcnt waits count only the ring's direct loads.
   // Waiting here also lets the first tiles, issued before Q, arrive.
 #pragma unroll
-  for (int qb = 0; qb < kQB; ++qb)
-#pragma unroll
-    for (int kk = 0; kk < kD / 16; ++kk) asm volatile("" ::"v"(qf[qb][kk]));
+  for (int kk = 0; kk < kD / 16; ++kk) asm volatile("" ::"v"(qf[kk]));
 #pragma unroll
   for (int k = 0; k < kNodesPerLane; ++k) asm volatile("" ::"v"(my_parent[k]));
 
@@ -354,15 +345,10 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   }
 
   // ---- online softmax state (raw score units) and O^T accumulators
-  float m_run[kQB], l_run[kQB];
-  f32x16 o_acc[kQB][kD / 32];
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x16 o_acc[kD / 32];
 #pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
-    m_run[qb] = -INFINITY;
-    l_run[qb] = 0.f;
-#pragma unroll
-    for (int db = 0; db < kD / 32; ++db) o_acc[qb][db] = f32x16{};
-  }
+  for (int db = 0; db < kD / 32; ++db) o_acc[db] = f32x16{};
   const float c = a.scale_log2;
 
   // LDS read offsets (bytes within a tile), all loop-invariant:
@@ -383,104 +369,89 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     v_rd[db] = tr_key * (kD * 2) + (((dim >> 3) ^ swz_v(tr_key)) << 4) + (dim & 7) * 2;
   }
 
-  for (int t = 0; t < n_tiles; ++t) {
-    const int ahead = min(kStages - 2, n_tiles - 1 - t);  // tiles in flight behind tile t
-    if (ahead >= 3) wait_vmcnt<3 * kLoadsPerTile>();
-    else if (ahead == 2) wait_vmcnt<2 * kLoadsPerTile>();
-    else if (ahead == 1) wait_vmcnt<kLoadsPerTile>();
-    else wait_vmcnt<0>();
-    barrier_only();  // tile t landed for all waves; every wave is done with tile t-1
-    if (t + kStages - 1 < n_tiles) issue_tile(t + kStages - 1);
-
+  // K fragments of a tile (A operand of S^T), read into registers one phase
+  // ahead of their MFMAs.
+  bf16x8 af[2][kD / 16];
+  auto load_k = [&](int t) {
     const unsigned char* k_s = sm.kv[t % kStages];
-    const unsigned char* v_s = k_s + kKBytes;
+#pragma unroll
+    for (int kk = 0; kk < kD / 16; ++kk)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        af[kb][kk] = *reinterpret_cast<const bf16x8*>(k_s + kb * 32 * (kD * 2) + k_rd[kk]);
+  };
+  // S^T = K Q^T from the fragments in af, the two 32-key blocks interleaved.
+  auto scores = [&](f32x16(&s)[2]) {
+    s[0] = s[1] = f32x16{};
+#pragma unroll
+    for (int kk = 0; kk < kD / 16; ++kk)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kb][kk], qf[kk], s[kb], 0, 0, 0);
+  };
+
+  // Masks and the online softmax of tile t; writes the P^T fragments.
+  auto softmax = [&](int t, f32x16(&s)[2], bf16x8(&pf)[2][2]) {
     const int tile0 = t * kKT;
-
-    // ---- S^T = K Q^T, the two 32-key blocks interleaved
-    f32x16 s_acc[kQB][2];
-#pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) s_acc[qb][0] = s_acc[qb][1] = f32x16{};
-#pragma unroll
-    for (int k4 = 0; k4 < kD / 64; ++k4) {
-      bf16x8 af[2][4];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          af[kb][u] =
-              *reinterpret_cast<const bf16x8*>(k_s + kb * 32 * (kD * 2) + k_rd[4 * k4 + u]);
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int qb = 0; qb < kQB; ++qb)
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb)
-            s_acc[qb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kb][u], qf[qb][4 * k4 + u],
-                                                                    s_acc[qb][kb], 0, 0, 0);
-    }
-
-    // ---- masks, online softmax, P^T fragments
-    const bool tail = tile0 + kKT > n_keys;
-    bf16x8 pf[kQB][2][2];
-#pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) {
-      if (kTree || tail) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          const int kfirst = tile0 + kb * 32 + 16 * h;  // key of register r = kfirst + r
-          uint32_t vis = 0xFFFFu;
-          if (kfirst + 16 > n_keys)
-            vis = (kfirst >= n_keys) ? 0u : ((1u << (n_keys - kfirst)) - 1u);
-          if (kTree) vis &= (sm.anc[qnode[qb]][(tile0 + kb * 32) >> 5] >> (16 * h)) & 0xFFFFu;
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (!((vis >> r) & 1u)) s_acc[qb][kb][r] = -INFINITY;
-        }
-      }
-      float tmax = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; r += 2)
-          tmax = __builtin_fmaxf(tmax, __builtin_fmaxf(s_acc[qb][kb][r], s_acc[qb][kb][r + 1]));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
-      // raise the reference max only when a score exceeds it by 2^kLazyMax
-      const float m_new = (tmax * c > m_run[qb] * c + kLazyMax || m_run[qb] == -INFINITY)
-                              ? fmaxf(m_run[qb], tmax)
-                              : m_run[qb];
-      const float neg = (m_new == -INFINITY) ? 0.f : -m_new * c;
-      float psum = 0.f;
+    if (kTree || tile0 + kKT > n_keys) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
+        const int kfirst = tile0 + kb * 32 + 16 * h;  // key of register r = kfirst + r
+        uint32_t vis = 0xFFFFu;
+        if (kfirst + 16 > n_keys) vis = (kfirst >= n_keys) ? 0u : ((1u << (n_keys - kfirst)) - 1u);
+        if (kTree) vis &= (sm.anc[qnode][(tile0 + kb * 32) >> 5] >> (16 * h)) & 0xFFFFu;
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-          float p[8];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            p[j] = exp2_fast(__builtin_fmaf(s_acc[qb][kb][8 * kk + j], c, neg));
-            psum += p[j];
-          }
-          u32x4 pk;
-          pk.x = pack_bf16x2(p[0], p[1]);
-          pk.y = pack_bf16x2(p[2], p[3]);
-          pk.z = pack_bf16x2(p[4], p[5]);
-          pk.w = pack_bf16x2(p[6], p[7]);
-          pf[qb][kb][kk] = __builtin_bit_cast(bf16x8, pk);
-        }
+        for (int r = 0; r < 16; ++r)
+          if (!((vis >> r) & 1u)) s[kb][r] = -INFINITY;
       }
-      // Rescale only when some lane's reference max moved.
-      if (__builtin_amdgcn_ballot_w64(m_new != m_run[qb]) != 0) {
-        const float alpha = (m_new == -INFINITY) ? 1.f : exp2_fast((m_run[qb] - m_new) * c);
-        l_run[qb] *= alpha;
-#pragma unroll
-        for (int db = 0; db < kD / 32; ++db) o_acc[qb][db] *= alpha;
-      }
-      l_run[qb] += psum;
-      m_run[qb] = m_new;
     }
+    // IEEE maximum (NaN-propagating) needs no operand canonicalisation and
+    // maps to three-input v_maximum3_f32.
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; r += 2)
+        tmax = __builtin_elementwise_maximum(tmax, __builtin_elementwise_maximum(s[kb][r], s[kb][r + 1]));
+    tmax = __builtin_elementwise_maximum(tmax, __shfl_xor(tmax, 32, kWave));
+    // raise the reference max only when a score exceeds it by 2^kLazyMax
+    const float m_new =
+        (tmax * c > m_run * c + kLazyMax || m_run == -INFINITY) ? fmaxf(m_run, tmax) : m_run;
+    const float neg = (m_new == -INFINITY) ? 0.f : -m_new * c;
+    float psum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        float p[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          p[j] = exp2_fast(__builtin_fmaf(s[kb][8 * kk + j], c, neg));
+          psum += p[j];
+        }
+        u32x4 pk;
+        pk.x = pack_bf16x2(p[0], p[1]);
+        pk.y = pack_bf16x2(p[2], p[3]);
+        pk.z = pack_bf16x2(p[4], p[5]);
+        pk.w = pack_bf16x2(p[6], p[7]);
+        pf[kb][kk] = __builtin_bit_cast(bf16x8, pk);
+      }
+    }
+    // Rescale only when some lane's reference max moved.
+    if (__builtin_amdgcn_ballot_w64(m_new != m_run) != 0) {
+      const float alpha = (m_new == -INFINITY) ? 1.f : exp2_fast((m_run - m_new) * c);
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < kD / 32; ++db) o_acc[db] *= alpha;
+    }
+    l_run += psum;
+    m_run = m_new;
+  };
 
-    // ---- O^T += V^T P^T; k-step kc = 2*kb + kk covers keys 32*kb + 16*h +
-    // 8*kk .. +7, read as two transposed 4-key reads.
+  // O^T += V^T P^T for tile t; k-step kc = 2*kb + kk covers keys 32*kb +
+  // 16*h + 8*kk .. +7, read as two transposed 4-key reads.
+  auto accumulate = [&](int t, const bf16x8(&pf)[2][2]) {
+    const unsigned char* v_s = sm.kv[t % kStages] + kKBytes;
 #pragma unroll
     for (int kc = 0; kc < 4; ++kc) {
       const int koff = (32 * (kc >> 1) + 8 * (kc & 1)) * (kD * 2);
@@ -489,16 +460,37 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
       for (int db = 0; db < kD / 32; ++db) {
         const s16x4 lo = lds_read_tr(v_s + v_rd[db] + koff);
         const s16x4 hi = lds_read_tr(v_s + v_rd[db] + koff + 4 * (kD * 2));
-        vf[db] =
-            __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        vf[db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       }
 #pragma unroll
-      for (int qb = 0; qb < kQB; ++qb)
-#pragma unroll
-        for (int db = 0; db < kD / 32; ++db)
-          o_acc[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db], pf[qb][kc >> 1][kc & 1],
-                                                                  o_acc[qb][db], 0, 0, 0);
+      for (int db = 0; db < kD / 32; ++db)
+        o_acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db], pf[kc >> 1][kc & 1], o_acc[db], 0, 0, 0);
     }
+  };
+
+  // ---- tile loop.  The barrier that publishes tile t+1 sits between the
+  // softmax and the P.V product of tile t, and the K fragments of tile t+1
+  // are read right after it: those LDS reads then overlap the P.V MFMAs of
+  // tile t instead of stalling the S MFMAs of tile t+1.  Tile t's V is still
+  // being read after that barrier, so loads run kAhead = kStages - 2 tiles
+  // ahead and never refill a slot that is in use.
+  constexpr int kAhead = kStages - 2;
+  static_assert(kAhead == 2, "the vmcnt waits below assume two tiles of look-ahead");
+  auto publish = [&](int t) {  // wait for tile t, publish it, start loading tile t + kAhead
+    if (t + 1 < n_tiles) wait_vmcnt<kLoadsPerTile>();  // tile t+1 may stay in flight
+    else wait_vmcnt<0>();
+    barrier_only();  // tile t landed for all waves; every wave is done with tile t-2
+    if (t + kAhead < n_tiles) issue_tile(t + kAhead);
+    load_k(t);
+  };
+  f32x16 s_acc[2];
+  bf16x8 pf[2][2];
+  if (n_tiles > 0) publish(0);
+  for (int t = 0; t < n_tiles; ++t) {
+    scores(s_acc);
+    softmax(t, s_acc, pf);
+    if (t + 1 < n_tiles) publish(t + 1);
+    accumulate(t, pf);
   }
 
   // ---- partial results of this split: (max in log2 units, sum) in fp32 and
@@ -507,27 +499,25 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   // pass through LDS so that every store writes whole rows: a wave's 32 rows
   // are one contiguous 8 KiB block of the workspace.
   constexpr int kRowPitch = kD * 2 + 16;  // padded LDS row (bank spread)
-  static_assert(kWaves * 32 * kQB * kRowPitch <= kStages * kTileBytes, "staging fits the ring");
+  static_assert(kWaves * 32 * kRowPitch <= kStages * kTileBytes, "staging fits the ring");
   const int64_t part = (static_cast<int64_t>(bg) * a.max_splits + split) * a.Mpad;
   barrier_only();  // every wave is done with the K/V ring; reuse it for staging
-  unsigned char* stage = &sm.kv[0][0] + wave * (32 * kRowPitch * kQB);  // spans ring slots
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
-    const float lsum = l_run[qb] + __shfl_xor(l_run[qb], 32, kWave);
-    const int row = row0 + (wave * kQB + qb) * 32 + l32;
-    if (row < valid_rows && h == 0) {
-      f32x2 ml = {m_run[qb] * c, lsum};
-      *reinterpret_cast<f32x2*>(a.ws_ml + (part + row) * 2) = ml;
+  unsigned char* stage = &sm.kv[0][0] + wave * (32 * kRowPitch);  // spans ring slots
+  {
+    const float lsum = l_run + __shfl_xor(l_run, 32, kWave);
+    if (qvalid && h == 0) {
+      f32x2 ml = {m_run * c, lsum};
+      *reinterpret_cast<f32x2*>(a.ws_ml + (part + qrow_idx) * 2) = ml;
     }
     const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-    unsigned char* srow = stage + (qb * 32 + l32) * kRowPitch;
+    unsigned char* srow = stage + l32 * kRowPitch;
 #pragma unroll
     for (int db = 0; db < kD / 32; ++db) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         uint2 v;
-        v.x = pack_bf16x2(o_acc[qb][db][4 * j] * inv, o_acc[qb][db][4 * j + 1] * inv);
-        v.y = pack_bf16x2(o_acc[qb][db][4 * j + 2] * inv, o_acc[qb][db][4 * j + 3] * inv);
+        v.x = pack_bf16x2(o_acc[db][4 * j] * inv, o_acc[db][4 * j + 1] * inv);
+        v.y = pack_bf16x2(o_acc[db][4 * j + 2] * inv, o_acc[db][4 * j + 3] * inv);
         *reinterpret_cast<uint2*>(srow + (db * 32 + 8 * j + 4 * h) * 2) = v;
       }
     }
@@ -535,8 +525,8 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  constexpr int kChunks = 32 * kQB * (kD * 2 / 16);  // 16-byte chunks of this wave's rows
-  const int wrow0 = row0 + wave * kQB * 32;
+  constexpr int kChunks = 32 * (kD * 2 / 16);  // 16-byte chunks of this wave's rows
+  const int wrow0 = row0 + wave * 32;
   unsigned char* gbase = reinterpret_cast<unsigned char*>(a.ws_o + (part + wrow0) * kD);
 #pragma unroll
   for (int i = 0; i < kChunks / kWave; ++i) {
