@@ -34,7 +34,7 @@
 //
 // The ancestor sets of the tree split are built in LDS as N x 256-bit masks by
 // pointer doubling over the parent links: anc(i) = anc(i) | anc(jump(i)),
-// jump(i) = jump(jump(i)), 8 rounds for N <= 256.
+// jump(i) = jump(jump(i)), ceil(log2(depth + 1)) <= 8 rounds for N <= 256.
 #include <algorithm>
 
 #include "ltd_device.hpp"
@@ -165,8 +165,7 @@ constexpr int kMaxSplitKeys = 960;     // <= kMaxSplitBlocks - 2 keys, a multipl
 struct Smem {
   unsigned char kv[kStages][kTileBytes];
   uint32_t anc[LTD_MAX_NODES][kAncWords];
-  uint32_t anc_tmp[LTD_MAX_NODES][kAncWords];  // second buffer of the mask build
-  int16_t jump[2][LTD_MAX_NODES];
+  int16_t jump[LTD_MAX_NODES];     // jump pointers of the mask build
   int32_t blk[kMaxSplitBlocks];  // physical block ids of this split's rows (paged)
 };
 
@@ -299,47 +298,59 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
 #pragma unroll
   for (int k = 0; k < kNodesPerLane; ++k) asm volatile("" ::"v"(my_parent[k]));
 
-  // ---- ancestor masks (tree split): wave 0 builds them by pointer doubling,
-  // anc(i) |= anc(jump(i)), jump(i) = jump(jump(i)), with wave-level ordering
-  // only; it stops once every jump pointer has passed the root (after
+  // ---- ancestor masks (tree split): wave 0 builds them by pointer doubling
+  // over the parent links, anc(i) |= anc(jump(i)), jump(i) = jump(jump(i)).
+  // Each lane keeps the sets and jump pointers of its nodes (i = lane + 64*k)
+  // in registers; a round publishes them to LDS, orders the wave's LDS
+  // traffic with one wave-level fence, and reads the jump targets' entries.
+  // The rounds stop once every jump pointer has passed the root (after
   // ceil(log2(depth + 1)) rounds).  The other waves go on to the tile loop,
   // whose first barrier publishes the masks.
   if (kTree && wave == 0) {
-    uint32_t* cur = &sm.anc[0][0];
-    uint32_t* nxt = &sm.anc_tmp[0][0];
+    typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
+    u32x8 anc_r[kNodesPerLane];
+    int jmp[kNodesPerLane];
+    const int nslots = (n + kWave - 1) / kWave;  // node slots holding a node of this tree
 #pragma unroll
     for (int k = 0; k < kNodesPerLane; ++k) {
       const int i = lane + kWave * k;
 #pragma unroll
-      for (int w = 0; w < kAncWords; ++w)
-        cur[i * kAncWords + w] = (i < n && (i >> 5) == w) ? (1u << (i & 31)) : 0u;
-      sm.jump[0][i] = static_cast<int16_t>(my_parent[k]);
+      for (int w = 0; w < kAncWords; ++w) anc_r[k][w] = (i < n && (i >> 5) == w) ? (1u << (i & 31)) : 0u;
+      jmp[k] = my_parent[k];
     }
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    u32x8* anc_lds = reinterpret_cast<u32x8*>(&sm.anc[0][0]);
     for (int r = 0; r < 8; ++r) {
-      const int jc = r & 1;
-      bool live = false;
 #pragma unroll
       for (int k = 0; k < kNodesPerLane; ++k) {
-        const int i = lane + kWave * k;
-        if (i < n) {
-          const int j = sm.jump[jc][i];
-#pragma unroll
-          for (int w = 0; w < kAncWords; ++w)
-            nxt[i * kAncWords + w] = cur[i * kAncWords + w] | (j >= 0 ? cur[j * kAncWords + w] : 0u);
-          const int jj = j >= 0 ? sm.jump[jc][j] : -1;
-          sm.jump[jc ^ 1][i] = static_cast<int16_t>(jj);
-          live |= jj >= 0;
+        if (k < nslots) {
+          const int i = lane + kWave * k;
+          anc_lds[i] = anc_r[k];
+          sm.jump[i] = static_cast<int16_t>(jmp[k]);
         }
       }
       __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-      uint32_t* t = cur;
-      cur = nxt;
-      nxt = t;
+      bool live = false;
+#pragma unroll
+      for (int k = 0; k < kNodesPerLane; ++k) {
+        if (k < nslots) {
+          const int j = jmp[k];
+          const int jc = j >= 0 ? j : 0;
+          const u32x8 other = anc_lds[jc];
+          const int jj = sm.jump[jc];
+          if (j >= 0) {
+            anc_r[k] |= other;
+            jmp[k] = jj;
+          }
+          live |= jmp[k] >= 0;
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
       if (__builtin_amdgcn_ballot_w64(live) == 0) break;
     }
-    if (cur != &sm.anc[0][0]) {
-      for (int i = lane; i < n * kAncWords; i += kWave) (&sm.anc[0][0])[i] = cur[i];
+#pragma unroll
+    for (int k = 0; k < kNodesPerLane; ++k) {
+      const int i = lane + kWave * k;
+      if (i < n) anc_lds[i] = anc_r[k];
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   }
@@ -497,7 +508,10 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   // the split's normalised output O / l in bf16 (half the bytes of raw fp32
   // partials; the merge weights each split by 2^(m - M) * l).  The O rows
   // pass through LDS so that every store writes whole rows: a wave's 32 rows
-  // are one contiguous 8 KiB block of the workspace.
+  // are one contiguous 8 KiB block of the workspace.  The stores are
+  // non-temporal: the merge kernel reads the partials from another XCD, so
+  // keeping them dirty in this XCD's L2 only lengthens the write-back at the
+  // end of the kernel.
   constexpr int kRowPitch = kD * 2 + 16;  // padded LDS row (bank spread)
   static_assert(kWaves * 32 * kRowPitch <= kStages * kTileBytes, "staging fits the ring");
   const int64_t part = (static_cast<int64_t>(bg) * a.max_splits + split) * a.Mpad;
@@ -507,7 +521,7 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     const float lsum = l_run + __shfl_xor(l_run, 32, kWave);
     if (qvalid && h == 0) {
       f32x2 ml = {m_run * c, lsum};
-      *reinterpret_cast<f32x2*>(a.ws_ml + (part + qrow_idx) * 2) = ml;
+      __builtin_nontemporal_store(ml, reinterpret_cast<f32x2*>(a.ws_ml + (part + qrow_idx) * 2));
     }
     const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
     unsigned char* srow = stage + l32 * kRowPitch;
@@ -533,8 +547,8 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     const int cidx = i * kWave + lane;
     const int r = cidx >> 4, col = cidx & 15;
     if (wrow0 + r < valid_rows)
-      *reinterpret_cast<u32x4*>(gbase + r * (kD * 2) + col * 16) =
-          *reinterpret_cast<const u32x4*>(stage + r * kRowPitch + col * 16);
+      __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(stage + r * kRowPitch + col * 16),
+                                  reinterpret_cast<u32x4*>(gbase + r * (kD * 2) + col * 16));
   }
 }
 
