@@ -95,8 +95,10 @@ extern "C" {
  *   Hq % Hkv == 0, d in {64, 128}, 1 <= Nmax <= LTD_MAX_NODES.
  *   scale       softmax scale (1/sqrt(d) for standard attention).
  *   workspace   device scratch of at least ltd_tree_verify_attn_workspace_size()
- *               bytes for the same (B, Nmax, Hq, Hkv, d, max_prefix, dtype); its
- *               contents need no initialisation and are garbage afterwards.
+ *               bytes for the same (B, Nmax, Hq, Hkv, d, max_prefix, dtype) (that
+ *               size covers every cache layout; it is 0 when no sequence can
+ *               need more than one KV split, and workspace may then be NULL);
+ *               its contents need no initialisation and are garbage afterwards.
  */
 size_t ltd_tree_verify_attn_workspace_size(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
                                            int dtype);
@@ -159,8 +161,11 @@ int ltd_kv_compact(void* k_cache, void* v_cache, const int32_t* block_table,
                    int64_t layer_stride_elems, int dtype, int validate, int32_t* status,
                    void* stream);
 
-/* Number of KV splits the attention launch uses for a sequence with prefix
- * length `prefix` (introspection for tests and benchmarks; -1 on bad args). */
+/* Number of KV splits (workgroups along the keys per sequence, kv head and
+ * row tile) the attention launch uses for a sequence with prefix length
+ * `prefix` in a contiguous cache; the last split also takes the tree's keys,
+ * and a single split writes the output without a merge pass (introspection
+ * for tests and benchmarks; -1 on bad args). */
 int ltd_tree_verify_attn_num_splits(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
                                     int dtype, int prefix);
 

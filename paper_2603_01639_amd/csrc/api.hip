@@ -51,7 +51,9 @@ const char* ltd_version(void) { return "ltd_verify 0.1 (gfx950)"; }
 size_t ltd_tree_verify_attn_workspace_size(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
                                            int dtype) {
   if (!attn_args_ok(B, Nmax, Hq, Hkv, d, max_prefix, dtype) || !attn_supported(d, dtype)) return 0;
-  const ltd::AttnShape s = make_shape(B, Nmax, Hq, Hkv, d, max_prefix, 1, 0, dtype);
+  // The layout with the most splits (paged, one row per block) bounds every
+  // layout's need.
+  const ltd::AttnShape s = make_shape(B, Nmax, Hq, Hkv, d, max_prefix, 1, 1, dtype);
   return ltd::plan_attention(s, device_cu_count()).workspace_bytes;
 }
 
@@ -63,7 +65,7 @@ int ltd_tree_verify_attn_num_splits(int B, int Nmax, int Hq, int Hkv, int d, int
   const ltd::AttnShape s = make_shape(B, Nmax, Hq, Hkv, d, max_prefix, 1, 0, dtype);
   const ltd::AttnPlan p = ltd::plan_attention(s, device_cu_count());
   if (!p.mfma) return 1;
-  return (prefix + p.split_keys - 1) / p.split_keys + 1;
+  return prefix == 0 ? 1 : (prefix + p.split_keys - 1) / p.split_keys;
 }
 
 int ltd_tree_verify_attn(const void* q, const void* k_cache, const void* v_cache,

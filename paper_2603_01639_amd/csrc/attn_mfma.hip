@@ -10,11 +10,12 @@
 //   S^T[key][row] = K[key][:] . Q[row][:]        (v_mfma_f32_32x32x16_bf16)
 //   O^T[dim][row] += V^T[dim][key] . P^T[key][row]
 //
-// Work split: grid = (KV split, row tile, b*Hkv + g).  A workgroup of 8
-// wavefronts owns 8*32*QB stacked rows (32*QB per wave) and one KV split: a
-// range of prefix keys or - for the last split - the tree's own N keys under
-// the ancestor mask.  Each split writes an unnormalised partial (running max
-// m, sum l, O) that attn_merge_kernel combines.
+// Work split: grid = (b*Hkv + g, row tile, KV split).  A workgroup of 8
+// wavefronts owns 8*32 stacked rows (32 per wave) and one KV split: a range of
+// prefix keys, and for the last split of a (sequence, kv head) also the
+// tree's own N keys under the ancestor mask.  With several splits each one
+// writes a partial result (its max, sum and normalised output) that
+// attn_merge_kernel combines; a single split writes the output directly.
 //
 // K/V stream: 64-key tiles move from HBM straight into an LDS ring of
 // kStages slots with global_load_lds_dwordx4 (no register staging); a lane
@@ -109,8 +110,10 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
-__device__ __forceinline__ int n_prefix_splits(int P, int split_keys) {
-  return (P + split_keys - 1) / split_keys;
+// KV splits of a sequence with prefix P: ceil(P / split_keys), at least one;
+// the last one also takes the tree's keys.
+__device__ __forceinline__ int n_splits_of(int P, int split_keys) {
+  return max(1, (P + split_keys - 1) / split_keys);
 }
 
 __device__ __forceinline__ lds_void* as_lds(const void* p) { return (lds_void*)(p); }
@@ -160,7 +163,13 @@ __device__ __forceinline__ void dma16(uint32_t lds, const void* lane_ptr) {
 __device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
 
 constexpr int kMaxSplitBlocks = 1024;  // paged block ids one split may span
-constexpr int kMaxSplitKeys = 960;     // <= kMaxSplitBlocks - 2 keys, a multiple of kKT
+#ifndef LTD_MAX_SPLIT_TILES
+#define LTD_MAX_SPLIT_TILES 32
+#endif
+// Longest split in key tiles: keeps any one workgroup's chain of tiles short
+// next to the whole grid's work when sequences of different lengths are
+// batched (a longer split would leave its compute unit the last one busy).
+constexpr int kMaxSplitTiles = LTD_MAX_SPLIT_TILES;
 
 struct Smem {
   unsigned char kv[kStages][kTileBytes];
@@ -192,35 +201,55 @@ __device__ __forceinline__ LoadPlan make_load_plan(int wave, int lane) {
   return lp;
 }
 
-// The attention of one workgroup over one KV split.
+// The attention of one workgroup over one KV split: the prefix keys
+// [key_begin, key_begin + n_pre) and, for the last split of a (sequence, kv
+// head) (kTree), also the tree's keys [P, P + n) under the ancestor mask.
+// Tiles t < tA cover the first range, the rest the second; a tile never spans
+// both.  With a single split the workgroup writes the final output.
 template <bool kTree>
 __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g, int bg, int split,
-                                       int row0, int valid_rows, int key_begin, int n_keys) {
+                                       int n_splits, int row0, int valid_rows, int key_begin,
+                                       int n_pre, int P) {
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
   const int lane = tid % kWave;
   const int h = lane >> 5;
   const int l32 = lane & 31;
   const int n = a.n_nodes[b];
+  const int n_tree = kTree ? n : 0;  // keys of the second range
+  const int tA = (n_pre + kKT - 1) / kKT;
+  const int n_tiles = tA + (n_tree + kKT - 1) / kKT;
+  // Tile t: its first logical cache row, the keys of its range from there on
+  // (more than kKT for all but a range's last tile), and whether it is a tree
+  // tile (then `rel` is its first key relative to P).
+  struct TileRef {
+    int row, left, rel;
+    bool tree;
+  };
+  auto tile_ref = [&](int t) -> TileRef {
+    if (!kTree || t < tA) return TileRef{key_begin + t * kKT, n_pre - t * kKT, 0, false};
+    const int rel = (t - tA) * kKT;
+    return TileRef{P + rel, n_tree - rel, rel, true};
+  };
 
   // ---- direct K/V tile loads
   const LoadPlan lp = make_load_plan(wave, lane);
   const unsigned char* kbase = reinterpret_cast<const unsigned char*>(a.k);
   const unsigned char* vbase = reinterpret_cast<const unsigned char*>(a.v);
   const bool paged = a.block_table != nullptr;
-  const int n_tiles = (n_keys + kKT - 1) / kKT;
   // Paged caches: this split's block ids are staged in LDS first, so address
-  // generation never waits on a global load.
+  // generation never waits on a global load.  The split's rows are one
+  // contiguous logical range (for the last split the tree rows follow the
+  // prefix rows directly).
   int first_blk = 0;
   if (paged) {
     first_blk = key_begin / a.kv_rows;
-    const int n_blk = (key_begin + n_keys - 1) / a.kv_rows - first_blk + 1;
+    const int n_blk = (key_begin + n_pre + n_tree - 1) / a.kv_rows - first_blk + 1;
     const int32_t* bt = a.block_table + static_cast<int64_t>(b) * a.max_blocks + first_blk;
     for (int j = tid; j < n_blk; j += kThreads) sm.blk[j] = bt[j];
     __syncthreads();
   }
-  auto row_byte = [&](int key_in_split) -> int64_t {  // byte offset of a cache row
-    const int row = key_begin + key_in_split;
+  auto row_byte = [&](int row) -> int64_t {  // byte offset of logical cache row `row`
     if (!paged) return ((static_cast<int64_t>(b) * a.Hkv + g) * a.kv_rows + row) * (kD * 2);
     const int64_t blk = sm.blk[row / a.kv_rows - first_blk];
     return ((blk * a.Hkv + g) * a.kv_rows + row % a.kv_rows) * (kD * 2);
@@ -234,22 +263,22 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   auto issue_tile = [&](int t) {
     const unsigned char* k_s = sm.kv[t % kStages];
     const unsigned char* v_s = k_s + kKBytes;
-    const int tile0 = t * kKT;
-    if (!paged && tile0 + kKT <= n_keys) {
+    const TileRef tr = tile_ref(t);
+    if (!paged && tr.left >= kKT) {
       // contiguous rows: a uniform tile base plus per-lane 32-bit offsets
-      const int64_t base = row_byte(tile0);
+      const int64_t base = row_byte(tr.row);
 #pragma unroll
       for (int u = 0; u < kKLoads; ++u) {
         dma16(lds_addr(k_s + lp.lds_pos[u]), kbase + base, k_voff[u]);
         dma16(lds_addr(v_s + lp.lds_pos[u]), vbase + base, v_voff[u]);
       }
     } else {
-      // paged rows, or the split's last partial tile (keys past the end read
-      // the last key's row and are masked out)
+      // paged rows, or a range's last partial tile (keys past the range's end
+      // read its last row and are masked out)
 #pragma unroll
       for (int u = 0; u < kKLoads; ++u) {
-        const int kk = min(tile0 + lp.k_key[u], n_keys - 1);
-        const int vk = min(tile0 + lp.v_key[u], n_keys - 1);
+        const int kk = tr.row + min(lp.k_key[u], tr.left - 1);
+        const int vk = tr.row + min(lp.v_key[u], tr.left - 1);
         dma16(lds_addr(k_s + lp.lds_pos[u]), kbase + row_byte(kk) + lp.k_off[u]);
         dma16(lds_addr(v_s + lp.lds_pos[u]), vbase + row_byte(vk) + lp.v_off[u]);
       }
@@ -266,6 +295,9 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   bf16x8 qf[kD / 16];
   const int qrow_idx = row0 + wave * 32 + l32;
   const bool qvalid = qrow_idx < valid_rows;
+  // A wave whose 32 rows are all padding only loads tiles and takes part in
+  // the barriers.
+  const bool active = row0 + wave * 32 < valid_rows;
   const int qnode = qvalid ? qrow_idx / a.G : 0;
   {
     const int hg = qvalid ? qrow_idx % a.G : 0;
@@ -403,14 +435,14 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
 
   // Masks and the online softmax of tile t; writes the P^T fragments.
   auto softmax = [&](int t, f32x16(&s)[2], bf16x8(&pf)[2][2]) {
-    const int tile0 = t * kKT;
-    if (kTree || tile0 + kKT > n_keys) {
+    const TileRef tr = tile_ref(t);
+    if (tr.tree || tr.left < kKT) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const int kfirst = tile0 + kb * 32 + 16 * h;  // key of register r = kfirst + r
+        const int kfirst = kb * 32 + 16 * h;  // tile key of register r = kfirst + r
         uint32_t vis = 0xFFFFu;
-        if (kfirst + 16 > n_keys) vis = (kfirst >= n_keys) ? 0u : ((1u << (n_keys - kfirst)) - 1u);
-        if (kTree) vis &= (sm.anc[qnode][(tile0 + kb * 32) >> 5] >> (16 * h)) & 0xFFFFu;
+        if (kfirst + 16 > tr.left) vis = (kfirst >= tr.left) ? 0u : ((1u << (tr.left - kfirst)) - 1u);
+        if (tr.tree) vis &= (sm.anc[qnode][(tr.rel + kb * 32) >> 5] >> (16 * h)) & 0xFFFFu;
 #pragma unroll
         for (int r = 0; r < 16; ++r)
           if (!((vis >> r) & 1u)) s[kb][r] = -INFINITY;
@@ -492,34 +524,39 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     else wait_vmcnt<0>();
     barrier_only();  // tile t landed for all waves; every wave is done with tile t-2
     if (t + kAhead < n_tiles) issue_tile(t + kAhead);
-    load_k(t);
+    if (active) load_k(t);
   };
   f32x16 s_acc[2];
   bf16x8 pf[2][2];
   if (n_tiles > 0) publish(0);
   for (int t = 0; t < n_tiles; ++t) {
-    scores(s_acc);
-    softmax(t, s_acc, pf);
+    if (active) {
+      scores(s_acc);
+      softmax(t, s_acc, pf);
+    }
     if (t + 1 < n_tiles) publish(t + 1);
-    accumulate(t, pf);
+    if (active) accumulate(t, pf);
   }
 
-  // ---- partial results of this split: (max in log2 units, sum) in fp32 and
-  // the split's normalised output O / l in bf16 (half the bytes of raw fp32
-  // partials; the merge weights each split by 2^(m - M) * l).  The O rows
-  // pass through LDS so that every store writes whole rows: a wave's 32 rows
-  // are one contiguous 8 KiB block of the workspace.  The stores are
-  // non-temporal: the merge kernel reads the partials from another XCD, so
-  // keeping them dirty in this XCD's L2 only lengthens the write-back at the
-  // end of the kernel.
+  // ---- results.  With one split the normalised output O / l goes straight
+  // to `out`.  Otherwise the split's partial result: (max in log2 units, sum)
+  // in fp32 and O / l in bf16 (half the bytes of raw fp32 partials; the merge
+  // weights each split by 2^(m - M) * l).  The O rows pass through LDS so that
+  // every store writes whole 256-byte rows (a wave's 32 partial rows are one
+  // contiguous 8 KiB block of the workspace).  Partials are stored
+  // non-temporally: the merge kernel reads them from another XCD, so keeping
+  // them dirty in this XCD's L2 only lengthens the write-back at the end of
+  // the kernel.
   constexpr int kRowPitch = kD * 2 + 16;  // padded LDS row (bank spread)
   static_assert(kWaves * 32 * kRowPitch <= kStages * kTileBytes, "staging fits the ring");
+  const bool final_out = n_splits == 1;
   const int64_t part = (static_cast<int64_t>(bg) * a.max_splits + split) * a.Mpad;
   barrier_only();  // every wave is done with the K/V ring; reuse it for staging
+  if (!active) return;
   unsigned char* stage = &sm.kv[0][0] + wave * (32 * kRowPitch);  // spans ring slots
   {
     const float lsum = l_run + __shfl_xor(l_run, 32, kWave);
-    if (qvalid && h == 0) {
+    if (!final_out && qvalid && h == 0) {
       f32x2 ml = {m_run * c, lsum};
       __builtin_nontemporal_store(ml, reinterpret_cast<f32x2*>(a.ws_ml + (part + qrow_idx) * 2));
     }
@@ -541,10 +578,31 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   constexpr int kChunks = 32 * (kD * 2 / 16);  // 16-byte chunks of this wave's rows
   const int wrow0 = row0 + wave * 32;
+  // (an opaque copy of the lane index: otherwise the compiler shares the
+  // chunk indices below with the parent-link loads before the tile loop and
+  // keeps them live, and spills them, across it)
+  int lane_e = lane;
+  asm volatile("" : "+v"(lane_e));
+  if (final_out) {
+    // stacked row r = node * G + head in group -> out[b][node][g * G + head]
+#pragma unroll
+    for (int i = 0; i < kChunks / kWave; ++i) {
+      const int cidx = i * kWave + lane_e;
+      const int r = cidx >> 4, col = cidx & 15;
+      const int row = wrow0 + r;
+      if (row < valid_rows) {
+        uint16_t* orow =
+            a.out + ((static_cast<int64_t>(b) * a.Nmax + row / a.G) * a.Hq + g * a.G + row % a.G) * kD;
+        *reinterpret_cast<u32x4*>(orow + col * 8) =
+            *reinterpret_cast<const u32x4*>(stage + r * kRowPitch + col * 16);
+      }
+    }
+    return;
+  }
   unsigned char* gbase = reinterpret_cast<unsigned char*>(a.ws_o + (part + wrow0) * kD);
 #pragma unroll
   for (int i = 0; i < kChunks / kWave; ++i) {
-    const int cidx = i * kWave + lane;
+    const int cidx = i * kWave + lane_e;
     const int r = cidx >> 4, col = cidx & 15;
     if (wrow0 + r < valid_rows)
       __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(stage + r * kRowPitch + col * 16),
@@ -554,24 +612,28 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
 
 __global__ void __launch_bounds__(kThreads, 1) attn_mfma_kernel(MfmaArgs a) {
   __shared__ __attribute__((aligned(16))) Smem sm;
-  const int split = blockIdx.x;
+  // (sequence, kv head) is the fastest grid dimension: workgroups are dealt
+  // to the 8 XCDs by linear id modulo 8, so each kv head's splits and row
+  // tiles share one XCD (its L2 holds their common Q rows and K/V), and the
+  // XCDs receive equal shares of every split index.
+  const int bg = blockIdx.x;
   const int rtile = blockIdx.y;
-  const int bg = blockIdx.z;
+  const int split = blockIdx.z;
   const int b = bg / a.Hkv;
   const int g = bg % a.Hkv;
   if (halted(a.status)) return;
   const int P = a.prefix_len[b];
   const int n = a.n_nodes[b];
-  const int nps = n_prefix_splits(P, a.split_keys);
-  if (split > nps) return;
+  const int nsp = n_splits_of(P, a.split_keys);
+  if (split >= nsp) return;
   const int valid_rows = a.G * n;
   const int row0 = rtile * kTileRows;
   if (row0 >= valid_rows) return;
-  if (split == nps)
-    attend<true>(a, sm, b, g, bg, split, row0, valid_rows, P, n);
+  const int key_begin = split * a.split_keys;
+  if (split == nsp - 1)
+    attend<true>(a, sm, b, g, bg, split, nsp, row0, valid_rows, key_begin, P - key_begin, P);
   else
-    attend<false>(a, sm, b, g, bg, split, row0, valid_rows, split * a.split_keys,
-                  min(P - split * a.split_keys, a.split_keys));
+    attend<false>(a, sm, b, g, bg, split, nsp, row0, valid_rows, key_begin, a.split_keys, P);
 }
 
 // One wave per stacked row: combine the splits' partials
@@ -582,18 +644,19 @@ __global__ void __launch_bounds__(kThreads, 1) attn_mfma_kernel(MfmaArgs a) {
 // flight per load, and the groups' sums are added with two lane exchanges.
 __global__ void __launch_bounds__(256) attn_merge_kernel(MfmaArgs a) {
   __shared__ float w_s[4][kMaxMergeSplits];
-  const int bg = blockIdx.y;
+  const int bg = blockIdx.x;
   const int b = bg / a.Hkv;
   const int g = bg % a.Hkv;
   if (halted(a.status)) return;
   const int wv = threadIdx.x / kWave;
-  const int row = blockIdx.x * 4 + wv;
+  const int row = blockIdx.y * 4 + wv;
   const int lane = threadIdx.x % kWave;
   const int n = a.n_nodes[b];
   if (row >= a.G * n) return;
   // (clamped so that a prefix above the planned maximum cannot index past the
   // workspace; such input is malformed and caught when validation is on)
-  const int n_splits = min(n_prefix_splits(a.prefix_len[b], a.split_keys) + 1, a.max_splits);
+  const int n_splits = min(n_splits_of(a.prefix_len[b], a.split_keys), a.max_splits);
+  if (n_splits == 1) return;  // the attention kernel wrote this row's output
   const int64_t part0 = static_cast<int64_t>(bg) * a.max_splits * a.Mpad + row;
   float M = -INFINITY;
   for (int s = lane; s < n_splits; s += kWave) M = fmaxf(M, a.ws_ml[(part0 + s * a.Mpad) * 2]);
@@ -655,9 +718,30 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(MfmaArgs a) {
 
 }  // namespace
 
+// Longest split (in keys, a multiple of the key tile) whose paged block ids
+// fit the LDS table: the last split's rows (its prefix keys plus up to Nmax
+// tree keys) span at most (keys + Nmax) / kv_rows + 2 blocks.  A contiguous
+// cache has no such bound.
+int64_t split_key_cap(const AttnShape& s) {
+  if (s.max_blocks <= 0) return int64_t{1} << 40;
+  const int64_t cap = static_cast<int64_t>(kMaxSplitBlocks - 2) * s.kv_rows - s.Nmax;
+  return cap / kKT * kKT;
+}
+
+// The smallest cap over every cache layout (paged with 1-row blocks); the
+// supported range and the workspace size use it, so that neither depends on
+// the layout of the call.
+int64_t worst_split_key_cap(const AttnShape& s) {
+  AttnShape w = s;
+  w.kv_rows = 1;
+  w.max_blocks = 1;
+  return split_key_cap(w);
+}
+
 bool mfma_supported(const AttnShape& s) {
-  return s.dtype == LTD_DTYPE_BF16 && s.d == kD &&
-         s.max_prefix <= static_cast<int64_t>(kMaxSplitKeys) * (kMaxMergeSplits - 1);
+  const int64_t cap = worst_split_key_cap(s);
+  return s.dtype == LTD_DTYPE_BF16 && s.d == kD && cap >= 2 * kKT &&
+         s.max_prefix <= cap * kMaxMergeSplits;
 }
 
 void plan_mfma(const AttnShape& s, int num_cus, AttnPlan* p) {
@@ -665,26 +749,26 @@ void plan_mfma(const AttnShape& s, int num_cus, AttnPlan* p) {
   p->rows = G * s.Nmax;
   p->tile_rows = kTileRows;
   p->row_tiles = (p->rows + kTileRows - 1) / kTileRows;
-  // Aim for kWgsPerCu resident workgroups per compute unit across the
-  // (sequence, kv head, row tile, split) grid; splits hold at least two tiles
-  // and the merge kernel's table bounds their number.
-  // Workgroups of a (sequence, kv head, row tile) unit: its prefix splits plus
-  // the tree split.  When all units fit one round of resident workgroups, the
-  // split count is chosen so that the whole grid still does: a second, nearly
-  // empty round would double the kernel time.
+  // A (sequence, kv head, row tile) unit is split along the keys into as
+  // many workgroups as keep one resident round of kWgsPerCu workgroups per
+  // compute unit busy (a second, nearly empty round would double the kernel
+  // time).  A split holds at least two key tiles, at most the paged table's
+  // cap, and the merge kernel's table bounds the number of splits.
   const int64_t units = static_cast<int64_t>(s.B) * s.Hkv * p->row_tiles;
   const int64_t target = static_cast<int64_t>(kWgsPerCu) * num_cus;
-  const int64_t want = std::max<int64_t>(1, target / units - 1);
-  int sk = static_cast<int>((s.max_prefix + want - 1) / want);
-  sk = std::max(sk, (s.max_prefix + kMaxMergeSplits - 2) / (kMaxMergeSplits - 1));
-  sk = ((sk + kKT - 1) / kKT) * kKT;
-  // At most kMaxSplitKeys keys per split, so that a split's paged block ids
-  // fit the LDS table for any block size.
-  p->split_keys = std::min(std::max(sk, 2 * kKT), kMaxSplitKeys);
-  p->max_splits = (s.max_prefix + p->split_keys - 1) / p->split_keys + 1;
+  const int64_t want = std::max<int64_t>(1, target / units);
+  int64_t sk = (s.max_prefix + want - 1) / want;
+  sk = std::max<int64_t>(sk, (s.max_prefix + kMaxMergeSplits - 1) / kMaxMergeSplits);
+  sk = std::max<int64_t>((sk + kKT - 1) / kKT * kKT, 2 * kKT);
+  sk = std::min<int64_t>(sk, static_cast<int64_t>(kMaxSplitTiles) * kKT);
+  sk = std::min(sk, split_key_cap(s));
+  p->split_keys = static_cast<int>(sk);
+  p->max_splits = static_cast<int>(std::max<int64_t>(1, (s.max_prefix + sk - 1) / sk));
+  // Partials exist only when some sequence can have more than one split.
   const int64_t Mpad = static_cast<int64_t>(p->row_tiles) * kTileRows;
   const int64_t slots = static_cast<int64_t>(s.B) * s.Hkv * p->max_splits * Mpad;
-  p->workspace_bytes = static_cast<size_t>(slots) * (kD * sizeof(uint16_t) + 2 * sizeof(float));
+  p->workspace_bytes =
+      p->max_splits > 1 ? static_cast<size_t>(slots) * (kD * sizeof(uint16_t) + 2 * sizeof(float)) : 0;
   p->mfma = true;
 }
 
@@ -717,11 +801,13 @@ hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q
   a.split_keys = p.split_keys;
   a.max_splits = p.max_splits;
   a.scale_log2 = scale * kLog2e;
-  const dim3 grid(p.max_splits, p.row_tiles, s.B * s.Hkv);
+  const dim3 grid(s.B * s.Hkv, p.row_tiles, p.max_splits);
   hipLaunchKernelGGL(attn_mfma_kernel, grid, dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const dim3 mgrid(static_cast<unsigned>((Mpad + 3) / 4), s.B * s.Hkv);
+  if (e != hipSuccess || p.max_splits == 1) return e;  // one split: the output is final
+  // (sequence, kv head) fastest, as for the attention grid: a head's merge
+  // runs on the XCD whose workgroups wrote its partials.
+  const dim3 mgrid(s.B * s.Hkv, static_cast<unsigned>((Mpad + 3) / 4));
   hipLaunchKernelGGL(attn_merge_kernel, mgrid, dim3(256), 0, stream, a);
   return hipGetLastError();
 }

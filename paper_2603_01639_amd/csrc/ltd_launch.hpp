@@ -26,7 +26,7 @@ struct AttnPlan {
   int row_tiles;   // workgroups along the stacked rows
   int tile_rows;   // rows per workgroup
   int split_keys;  // prefix keys per split (multiple of the key tile)
-  int max_splits;  // prefix splits for max_prefix, plus one split for the tree
+  int max_splits;  // KV splits for max_prefix (the last also takes the tree keys)
   bool mfma;       // bf16 MFMA split-KV path (else the row-wise VALU path)
   size_t workspace_bytes;
 };

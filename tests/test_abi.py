@@ -63,11 +63,19 @@ def test_binding_signatures_match_header():
 
 
 def test_bf16_head128_workloads_plan_the_mfma_split_path():
-    """The 8B/32B/70B-shaped bf16 shapes run on the MFMA split-KV kernels
-    (more than one split and a workspace), fp32 and d=64 on the row-wise one."""
-    for B, Nmax, Hq, Hkv, P in ((1, 60, 32, 8, 2048), (1, 60, 32, 8, 16384), (1, 256, 64, 8, 4096),
-                                (16, 128, 64, 8, 8192)):
+    """The 8B/32B-shaped bf16 shapes spread each (sequence, kv head) over
+    several KV splits (B=1 leaves most compute units idle otherwise).  The
+    16-sequence 70B-shaped batch already has more units than compute units;
+    its splits are only capped at 32 key tiles (2048 keys) so that no single
+    workgroup's chain of tiles dominates, and a sequence that fits one split
+    is written without a merge pass.  The workspace size covers the paged
+    layout with the most splits.  fp32 and d=64 run on the row-wise kernel."""
+    for B, Nmax, Hq, Hkv, P in ((1, 60, 32, 8, 2048), (1, 60, 32, 8, 16384), (1, 256, 64, 8, 4096)):
         assert ltd.attn_num_splits(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16, P) > 1
         assert ltd.attn_workspace_size(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16) > 0
+    assert ltd.attn_num_splits(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16, 8192) == 4
+    assert ltd.attn_num_splits(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16, 2048) == 1
+    assert ltd.attn_num_splits(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16, 0) == 1
+    assert ltd.attn_workspace_size(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16) > 0
     assert ltd.attn_num_splits(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32, 128) == 1
     assert ltd.attn_workspace_size(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32) == 0

@@ -5,6 +5,7 @@ import numpy as np
 import pytest
 
 import gpu_util as U
+import paper_2603_01639_amd as ltd
 from paper_2603_01639_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -145,3 +146,21 @@ def test_argmax_ties_signed_zero_and_ragged_vocab():
         got = U.gpu_accept(b, dev)
         want = U.check_accept(b, got)
         assert want[0][0, 0] == Voc // 2
+
+
+@pytest.mark.parametrize("block_size", [0, 16])
+def test_single_split_batch_writes_output_directly(block_size):
+    """A batch whose longest prefix fits one KV split: every (sequence, kv
+    head) is one workgroup that also takes the tree keys and writes the output
+    itself (no workspace, no merge pass), with rows spread over several row
+    tiles and padded rows in the last one."""
+    rng = np.random.default_rng(41 + block_size)
+    sizes = (40, 1, 33, 64, 17, 5, 28, 60, 9, 50, 3, 64)
+    trees = [W.tree_uniform_parent(rng, n) for n in sizes]
+    prefix = [int(p) for p in rng.integers(0, 129, size=len(sizes))]
+    prefix[1], prefix[4] = 0, 128
+    b = _custom(trees, prefix, Hq=32, Hkv=4, Nmax=64, block_size=block_size, seed=41,
+                label=f"single-split batch block={block_size}")
+    assert ltd.attn_workspace_size(b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix, b.dtype) == 0
+    assert ltd.attn_num_splits(b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix, b.dtype, b.max_prefix) == 1
+    _full_step(b)
