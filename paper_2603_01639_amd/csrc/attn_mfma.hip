@@ -110,6 +110,16 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// x of lane (l xor 32), with v_permlane32_swap (a VALU op; __shfl_xor goes
+// through the LDS crossbar, where it queues behind the tile's fragment reads).
+// The swap of x with itself leaves the upper half's values in the lower half
+// of the second result and the lower half's in the upper half of the first.
+__device__ __forceinline__ float xor32(float x) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __builtin_bit_cast(float, (__lane_id() & 32) ? r[0] : r[1]);
+}
+
 // KV splits of a sequence with prefix P: ceil(P / split_keys), at least one;
 // the last one also takes the tree's keys.
 __device__ __forceinline__ int n_splits_of(int P, int split_keys) {
@@ -433,8 +443,12 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kb][kk], qf[kk], s[kb], 0, 0, 0);
   };
 
-  // Masks and the online softmax of tile t; writes the P^T fragments.
-  auto softmax = [&](int t, f32x16(&s)[2], bf16x8(&pf)[2][2]) {
+  // The online softmax of a tile in three parts: the key mask (tiles that
+  // hold tree keys or end their range), the exponentials (writes the P^T
+  // fragments; the reference max m moves only when a score exceeds it by
+  // 2^kLazyMax) and the finish, which rescales O and l when some lane's m
+  // moved.  The finish must come after the previous tile's P.V product.
+  auto mask_scores = [&](int t, f32x16(&s)[2]) {
     const TileRef tr = tile_ref(t);
     if (tr.tree || tr.left < kKT) {
 #pragma unroll
@@ -448,6 +462,9 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
           if (!((vis >> r) & 1u)) s[kb][r] = -INFINITY;
       }
     }
+  };
+  float m_new = -INFINITY, psum = 0.f;
+  auto exponentials = [&](f32x16(&s)[2], bf16x8(&pf)[2][2]) {
     // IEEE maximum (NaN-propagating) needs no operand canonicalisation and
     // maps to three-input v_maximum3_f32.
     float tmax = -INFINITY;
@@ -456,12 +473,10 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
 #pragma unroll
       for (int r = 0; r < 16; r += 2)
         tmax = __builtin_elementwise_maximum(tmax, __builtin_elementwise_maximum(s[kb][r], s[kb][r + 1]));
-    tmax = __builtin_elementwise_maximum(tmax, __shfl_xor(tmax, 32, kWave));
-    // raise the reference max only when a score exceeds it by 2^kLazyMax
-    const float m_new =
-        (tmax * c > m_run * c + kLazyMax || m_run == -INFINITY) ? fmaxf(m_run, tmax) : m_run;
+    tmax = __builtin_elementwise_maximum(tmax, xor32(tmax));
+    m_new = (tmax * c > m_run * c + kLazyMax || m_run == -INFINITY) ? fmaxf(m_run, tmax) : m_run;
     const float neg = (m_new == -INFINITY) ? 0.f : -m_new * c;
-    float psum = 0.f;
+    float ps = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
@@ -470,7 +485,7 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           p[j] = exp2_fast(__builtin_fmaf(s[kb][8 * kk + j], c, neg));
-          psum += p[j];
+          ps += p[j];
         }
         u32x4 pk;
         pk.x = pack_bf16x2(p[0], p[1]);
@@ -480,7 +495,9 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
         pf[kb][kk] = __builtin_bit_cast(bf16x8, pk);
       }
     }
-    // Rescale only when some lane's reference max moved.
+    psum = ps;
+  };
+  auto finish_softmax = [&]() {
     if (__builtin_amdgcn_ballot_w64(m_new != m_run) != 0) {
       const float alpha = (m_new == -INFINITY) ? 1.f : exp2_fast((m_run - m_new) * c);
       l_run *= alpha;
@@ -511,12 +528,13 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     }
   };
 
-  // ---- tile loop.  The barrier that publishes tile t+1 sits between the
-  // softmax and the P.V product of tile t, and the K fragments of tile t+1
-  // are read right after it: those LDS reads then overlap the P.V MFMAs of
-  // tile t instead of stalling the S MFMAs of tile t+1.  Tile t's V is still
-  // being read after that barrier, so loads run kAhead = kStages - 2 tiles
-  // ahead and never refill a slot that is in use.
+  // ---- tile loop, software-pipelined by one phase: iteration t runs the
+  // P.V product of tile t-1 together with the softmax of tile t (one block
+  // of MFMAs and independent vector work for the scheduler to interleave),
+  // then publishes tile t+1, reads its K fragments and issues its S MFMAs.
+  // V of tile t-1 is still read in iteration t, so loads run kAhead =
+  // kStages - 2 tiles ahead and never refill a slot that is in use: the
+  // barrier that publishes tile t+1 comes after the last read of tile t-1.
   constexpr int kAhead = kStages - 2;
   static_assert(kAhead == 2, "the vmcnt waits below assume two tiles of look-ahead");
   auto publish = [&](int t) {  // wait for tile t, publish it, start loading tile t + kAhead
@@ -524,19 +542,35 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     else wait_vmcnt<0>();
     barrier_only();  // tile t landed for all waves; every wave is done with tile t-2
     if (t + kAhead < n_tiles) issue_tile(t + kAhead);
-    if (active) load_k(t);
   };
   f32x16 s_acc[2];
-  bf16x8 pf[2][2];
-  if (n_tiles > 0) publish(0);
-  for (int t = 0; t < n_tiles; ++t) {
+  bf16x8 pf[2][2], pf_prev[2][2];
+  if (n_tiles > 0) {
+    publish(0);
     if (active) {
+      load_k(0);
       scores(s_acc);
-      softmax(t, s_acc, pf);
+      mask_scores(0, s_acc);
+      exponentials(s_acc, pf);
+      finish_softmax();
     }
-    if (t + 1 < n_tiles) publish(t + 1);
-    if (active) accumulate(t, pf);
   }
+  for (int t = 1; t < n_tiles; ++t) {
+    publish(t);
+    if (active) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) pf_prev[kb][kk] = pf[kb][kk];
+      load_k(t);
+      scores(s_acc);
+      mask_scores(t, s_acc);
+      accumulate(t - 1, pf_prev);   // tile t-1's P.V ...
+      exponentials(s_acc, pf);      // ... interleaved with tile t's softmax
+      finish_softmax();             // after P.V(t-1): may rescale O
+    }
+  }
+  if (n_tiles > 0 && active) accumulate(n_tiles - 1, pf);
 
   // ---- results.  With one split the normalised output O / l goes straight
   // to `out`.  Otherwise the split's partial result: (max in log2 units, sum)
@@ -555,7 +589,7 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   if (!active) return;
   unsigned char* stage = &sm.kv[0][0] + wave * (32 * kRowPitch);  // spans ring slots
   {
-    const float lsum = l_run + __shfl_xor(l_run, 32, kWave);
+    const float lsum = l_run + xor32(l_run);
     if (!final_out && qvalid && h == 0) {
       f32x2 ml = {m_run * c, lsum};
       __builtin_nontemporal_store(ml, reinterpret_cast<f32x2*>(a.ws_ml + (part + qrow_idx) * 2));
