@@ -163,11 +163,13 @@ int ltd_kv_compact(void* k_cache, void* v_cache, const int32_t* block_table,
 
 /* Number of KV splits (workgroups along the keys per sequence, kv head and
  * row tile) the attention launch uses for a sequence with prefix length
- * `prefix` in a contiguous cache; the last split also takes the tree's keys,
- * and a single split writes the output without a merge pass (introspection
- * for tests and benchmarks; -1 on bad args). */
+ * `prefix` and `n_nodes` tree nodes in a contiguous cache.  The tree's keys
+ * go with the last prefix range or form a split of their own; a single split
+ * writes the output without a merge pass (introspection for tests and
+ * benchmarks; -1 on bad args, including prefix > max_prefix or
+ * n_nodes > Nmax). */
 int ltd_tree_verify_attn_num_splits(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
-                                    int dtype, int prefix);
+                                    int dtype, int prefix, int n_nodes);
 
 /* Library version string. */
 const char* ltd_version(void);

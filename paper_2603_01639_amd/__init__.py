@@ -75,7 +75,7 @@ def lib() -> ctypes.CDLL:
         L.ltd_tree_accept.restype = i32
         L.ltd_kv_compact.argtypes = [P] * 7 + [i32] * 8 + [i64, i32, i32, P, P]
         L.ltd_kv_compact.restype = i32
-        L.ltd_tree_verify_attn_num_splits.argtypes = [i32] * 8
+        L.ltd_tree_verify_attn_num_splits.argtypes = [i32] * 9
         L.ltd_tree_verify_attn_num_splits.restype = i32
         L.ltd_version.argtypes = []
         L.ltd_version.restype = ctypes.c_char_p
@@ -116,8 +116,9 @@ def attn_workspace_size(B, Nmax, Hq, Hkv, d, max_prefix, dtype) -> int:
     return int(lib().ltd_tree_verify_attn_workspace_size(B, Nmax, Hq, Hkv, d, max_prefix, dtype))
 
 
-def attn_num_splits(B, Nmax, Hq, Hkv, d, max_prefix, dtype, prefix) -> int:
-    return int(lib().ltd_tree_verify_attn_num_splits(B, Nmax, Hq, Hkv, d, max_prefix, dtype, prefix))
+def attn_num_splits(B, Nmax, Hq, Hkv, d, max_prefix, dtype, prefix, n_nodes) -> int:
+    return int(lib().ltd_tree_verify_attn_num_splits(B, Nmax, Hq, Hkv, d, max_prefix, dtype, prefix,
+                                                     n_nodes))
 
 
 def accept_workspace_size(B, Nmax, Voc) -> int:

@@ -58,14 +58,12 @@ size_t ltd_tree_verify_attn_workspace_size(int B, int Nmax, int Hq, int Hkv, int
 }
 
 int ltd_tree_verify_attn_num_splits(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
-                                    int dtype, int prefix) {
+                                    int dtype, int prefix, int n_nodes) {
   if (!attn_args_ok(B, Nmax, Hq, Hkv, d, max_prefix, dtype) || !attn_supported(d, dtype) ||
-      prefix < 0 || prefix > max_prefix)
+      prefix < 0 || prefix > max_prefix || n_nodes < 0 || n_nodes > Nmax)
     return -1;
   const ltd::AttnShape s = make_shape(B, Nmax, Hq, Hkv, d, max_prefix, 1, 0, dtype);
-  const ltd::AttnPlan p = ltd::plan_attention(s, device_cu_count());
-  if (!p.mfma) return 1;
-  return prefix == 0 ? 1 : (prefix + p.split_keys - 1) / p.split_keys;
+  return ltd::attention_splits(ltd::plan_attention(s, device_cu_count()), prefix, n_nodes);
 }
 
 int ltd_tree_verify_attn(const void* q, const void* k_cache, const void* v_cache,

@@ -94,7 +94,7 @@ struct MfmaArgs {
   uint16_t* out;
   const int32_t* status;
   int Nmax, Hq, Hkv, G, kv_rows, max_blocks;
-  int Mpad, split_keys, max_splits;
+  int Mpad, split_keys, max_splits, tree_alone;
   float scale_log2;
 };
 
@@ -120,10 +120,19 @@ __device__ __forceinline__ float xor32(float x) {
   return __builtin_bit_cast(float, (__lane_id() & 32) ? r[0] : r[1]);
 }
 
-// KV splits of a sequence with prefix P: ceil(P / split_keys), at least one;
-// the last one also takes the tree's keys.
-__device__ __forceinline__ int n_splits_of(int P, int split_keys) {
-  return max(1, (P + split_keys - 1) / split_keys);
+// KV splits of a sequence with prefix P and n tree nodes.  The prefix is cut
+// into ranges of split_keys keys (at least one range).  The tree's keys join
+// the last range, except when the plan sets tree_alone, the prefix has two or
+// more ranges and the last one would then hold more tiles than a full range:
+// the tree is then a split of its own, after the prefix ranges.
+__host__ __device__ __forceinline__ int n_splits_of(int P, int n, int split_keys, int tree_alone) {
+  const int pre = (P + split_keys - 1) / split_keys;
+  if (pre <= 1) return 1;
+  if (tree_alone) {
+    const int last_tiles = (P - (pre - 1) * split_keys + kKT - 1) / kKT;
+    if (last_tiles + (n + kKT - 1) / kKT > split_keys / kKT) return pre + 1;
+  }
+  return pre;
 }
 
 __device__ __forceinline__ lds_void* as_lds(const void* p) { return (lds_void*)(p); }
@@ -168,6 +177,11 @@ __device__ __forceinline__ void dma16(uint32_t lds, const void* lane_ptr) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(lane_ptr)
                : "memory");
 }
+// Direct global->LDS load of 4 bytes per lane (lane i's word lands at M0 + 4*i).
+__device__ __forceinline__ void dma4(uint32_t lds, const void* lane_ptr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(lds), "v"(lane_ptr)
+               : "memory");
+}
 // Workgroup barrier without the memory fence __syncthreads() adds (that fence
 // would also wait for every outstanding direct load).
 __device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
@@ -185,8 +199,12 @@ struct Smem {
   unsigned char kv[kStages][kTileBytes];
   uint32_t anc[LTD_MAX_NODES][kAncWords];
   int16_t jump[LTD_MAX_NODES];     // jump pointers of the mask build
+  int32_t par[LTD_MAX_NODES];      // the tree's parent links (mask build)
   int32_t blk[kMaxSplitBlocks];  // physical block ids of this split's rows (paged)
 };
+// The Q rows are loaded into ring slots 2 and 3 (8 KiB per wave) before the
+// first two tiles; the loop first writes those slots after its first barrier.
+static_assert(kStages >= 4 && 2 * kTileBytes >= kWaves * 32 * kD * 2, "Q fits ring slots 2-3");
 
 // This lane's share of a tile's direct loads: for load u (0..3) the tile row
 // of its K chunk and of its V chunk, the chunk's byte offset within the row,
@@ -242,6 +260,40 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     return TileRef{P + rel, n_tree - rel, rel, true};
   };
 
+  // ---- Q rows and parent links, straight into LDS ahead of everything else
+  // (the tile loads queue behind them, and the wait for them below leaves the
+  // first tiles in flight).  Wave w's 32 stacked rows row0 + 32w + R land at
+  // 256*R in its 8 KiB block, with 16-byte chunk c at c ^ (R & 15), the
+  // layout the K operand also uses; rows past valid_rows repeat the last
+  // valid row (their results are never stored).
+  const int qrow_idx = row0 + wave * 32 + l32;
+  const bool qvalid = qrow_idx < valid_rows;
+  // A wave whose 32 rows are all padding only loads tiles and takes part in
+  // the barriers.
+  const bool active = row0 + wave * 32 < valid_rows;
+  const int qnode = qvalid ? qrow_idx / a.G : 0;
+  unsigned char* q_lds = &sm.kv[2][0] + wave * (32 * kD * 2);
+  if (active) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int R = 4 * j + (lane >> 4);
+      const int idx = min(row0 + wave * 32 + R, valid_rows - 1);
+      const int lc = (lane & 15) ^ (R & 15);
+      const uint16_t* src = a.q +
+          ((static_cast<int64_t>(b) * a.Nmax + idx / a.G) * a.Hq + g * a.G + idx % a.G) * kD + lc * 8;
+      dma16(lds_addr(q_lds + j * 1024), src);
+    }
+  }
+  constexpr int kNodesPerLane = LTD_MAX_NODES / kWave;
+  const int nslots = (n + kWave - 1) / kWave;  // node slots holding a node of this tree
+  if (kTree && wave == 0) {
+#pragma unroll
+    for (int k = 0; k < kNodesPerLane; ++k)
+      if (k < nslots)
+        dma4(lds_addr(&sm.par[kWave * k]),
+             a.parents + static_cast<int64_t>(b) * a.Nmax + min(lane + kWave * k, n - 1));
+  }
+
   // ---- direct K/V tile loads
   const LoadPlan lp = make_load_plan(wave, lane);
   const unsigned char* kbase = reinterpret_cast<const unsigned char*>(a.k);
@@ -295,50 +347,39 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     }
   };
 
-  // First tiles in flight before anything else is loaded.
+  // The first tiles, behind Q.
 #pragma unroll
   for (int t = 0; t < kStages - 2; ++t)
     if (t < n_tiles) issue_tile(t);
+  // This wave's Q rows and parent links have landed once no more than the
+  // tiles' loads are outstanding.
+  if (n_tiles >= 2)
+    wait_vmcnt<2 * kLoadsPerTile>();
+  else if (n_tiles == 1)
+    wait_vmcnt<kLoadsPerTile>();
+  else
+    wait_vmcnt<0>();
 
   // ---- Q fragment (B operand of S^T): lane holds row l32 of the wave's
-  // 32-row block, dims 16*kk + 8*h .. +7.
+  // 32-row block, dims 16*kk + 8*h .. +7.  All waves have read theirs before
+  // the loop's first barrier, after which tile 2 overwrites the slot.
   bf16x8 qf[kD / 16];
-  const int qrow_idx = row0 + wave * 32 + l32;
-  const bool qvalid = qrow_idx < valid_rows;
-  // A wave whose 32 rows are all padding only loads tiles and takes part in
-  // the barriers.
-  const bool active = row0 + wave * 32 < valid_rows;
-  const int qnode = qvalid ? qrow_idx / a.G : 0;
-  {
-    const int hg = qvalid ? qrow_idx % a.G : 0;
-    const uint16_t* qrow =
-        a.q + ((static_cast<int64_t>(b) * a.Nmax + qnode) * a.Hq + g * a.G + hg) * kD;
+  if (active) {
 #pragma unroll
-    for (int kk = 0; kk < kD / 16; ++kk) {
-      u32x4 v = {0, 0, 0, 0};
-      if (qvalid) v = *reinterpret_cast<const u32x4*>(qrow + kk * 16 + 8 * h);
-      qf[kk] = __builtin_bit_cast(bf16x8, v);
-    }
+    for (int kk = 0; kk < kD / 16; ++kk)
+      qf[kk] = *reinterpret_cast<const bf16x8*>(q_lds + l32 * (kD * 2) +
+                                                (((2 * kk + h) ^ (l32 & 15)) << 4));
   }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 
   // The tree's parent links, for wave 0 (lane l handles nodes l + 64*k).
-  constexpr int kNodesPerLane = LTD_MAX_NODES / kWave;
   int my_parent[kNodesPerLane];
 #pragma unroll
   for (int k = 0; k < kNodesPerLane; ++k) {
     const int i = lane + kWave * k;
     my_parent[k] = -1;
-    if (kTree && wave == 0 && i > 0 && i < n)
-      my_parent[k] = a.parents[static_cast<int64_t>(b) * a.Nmax + i];
+    if (kTree && wave == 0 && i > 0 && i < n) my_parent[k] = sm.par[i];
   }
-
-  // The Q loads (and the tree's parent links) must have landed before the
-  // tile loop: its explicit vmcnt waits count only the ring's direct loads.
-  // Waiting here also lets the first tiles, issued before Q, arrive.
-#pragma unroll
-  for (int kk = 0; kk < kD / 16; ++kk) asm volatile("" ::"v"(qf[kk]));
-#pragma unroll
-  for (int k = 0; k < kNodesPerLane; ++k) asm volatile("" ::"v"(my_parent[k]));
 
   // ---- ancestor masks (tree split): wave 0 builds them by pointer doubling
   // over the parent links, anc(i) |= anc(jump(i)), jump(i) = jump(jump(i)).
@@ -352,7 +393,6 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
     u32x8 anc_r[kNodesPerLane];
     int jmp[kNodesPerLane];
-    const int nslots = (n + kWave - 1) / kWave;  // node slots holding a node of this tree
 #pragma unroll
     for (int k = 0; k < kNodesPerLane; ++k) {
       const int i = lane + kWave * k;
@@ -658,16 +698,19 @@ __global__ void __launch_bounds__(kThreads, 1) attn_mfma_kernel(MfmaArgs a) {
   if (halted(a.status)) return;
   const int P = a.prefix_len[b];
   const int n = a.n_nodes[b];
-  const int nsp = n_splits_of(P, a.split_keys);
+  const int nsp = n_splits_of(P, n, a.split_keys, a.tree_alone);
   if (split >= nsp) return;
   const int valid_rows = a.G * n;
   const int row0 = rtile * kTileRows;
   if (row0 >= valid_rows) return;
-  const int key_begin = split * a.split_keys;
+  // Prefix keys [key_begin, key_begin + n_pre); a tree split of its own
+  // starts at P with none.
+  const int key_begin = min(split * a.split_keys, P);
+  const int n_pre = min(a.split_keys, P - key_begin);
   if (split == nsp - 1)
-    attend<true>(a, sm, b, g, bg, split, nsp, row0, valid_rows, key_begin, P - key_begin, P);
+    attend<true>(a, sm, b, g, bg, split, nsp, row0, valid_rows, key_begin, n_pre, P);
   else
-    attend<false>(a, sm, b, g, bg, split, nsp, row0, valid_rows, key_begin, a.split_keys, P);
+    attend<false>(a, sm, b, g, bg, split, nsp, row0, valid_rows, key_begin, n_pre, P);
 }
 
 // One wave per stacked row: combine the splits' partials
@@ -689,7 +732,7 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(MfmaArgs a) {
   if (row >= a.G * n) return;
   // (clamped so that a prefix above the planned maximum cannot index past the
   // workspace; such input is malformed and caught when validation is on)
-  const int n_splits = min(n_splits_of(a.prefix_len[b], a.split_keys), a.max_splits);
+  const int n_splits = min(n_splits_of(a.prefix_len[b], n, a.split_keys, a.tree_alone), a.max_splits);
   if (n_splits == 1) return;  // the attention kernel wrote this row's output
   const int64_t part0 = static_cast<int64_t>(bg) * a.max_splits * a.Mpad + row;
   float M = -INFINITY;
@@ -778,31 +821,88 @@ bool mfma_supported(const AttnShape& s) {
          s.max_prefix <= cap * kMaxMergeSplits;
 }
 
+// Estimated time of one plan, in units of one key tile's time for a
+// workgroup: the rounds of resident workgroups times the longest split plus a
+// workgroup's fixed cost (loading Q, writing the result: about three tiles),
+// and the merge kernel when a sequence has several splits.  The sequence
+// priced is the longest the call allows (max_prefix keys, Nmax nodes).
+int attention_splits(const AttnPlan& p, int prefix, int n) {
+  if (!p.mfma) return 1;
+  return n_splits_of(prefix, n, p.split_keys, p.tree_alone ? 1 : 0);
+}
+
+static double plan_cost(int64_t P, int n, int64_t sk, bool alone, int64_t units, int64_t target) {
+  constexpr double kFixedTiles = 3.0, kMaskTiles = 0.5, kMergeTiles = 2.5;
+  const int64_t tps = sk / kKT;
+  const int64_t tree_tiles = (n + kKT - 1) / kKT;
+  const int64_t pre = (P + sk - 1) / sk;
+  const int S = n_splits_of(static_cast<int>(P), n, static_cast<int>(sk), alone);
+  double longest;
+  if (pre <= 1) {
+    longest = static_cast<double>((P + kKT - 1) / kKT + tree_tiles) + kMaskTiles;
+  } else {
+    const int64_t last = (P - (pre - 1) * sk + kKT - 1) / kKT;
+    const double tree_split =
+        static_cast<double>(S > pre ? tree_tiles : last + tree_tiles) + kMaskTiles;
+    longest = std::max(static_cast<double>(tps), tree_split);
+  }
+  const int64_t rounds = (units * S + target - 1) / target;
+  return static_cast<double>(rounds) * (longest + kFixedTiles) +
+         (S > 1 ? kMergeTiles + S / 32.0 : 0.0);
+}
+
 void plan_mfma(const AttnShape& s, int num_cus, AttnPlan* p) {
   const int G = s.Hq / s.Hkv;
   p->rows = G * s.Nmax;
   p->tile_rows = kTileRows;
   p->row_tiles = (p->rows + kTileRows - 1) / kTileRows;
-  // A (sequence, kv head, row tile) unit is split along the keys into as
-  // many workgroups as keep one resident round of kWgsPerCu workgroups per
+  // A (sequence, kv head, row tile) unit is split along the keys into about
+  // as many workgroups as keep one resident round of kWgsPerCu workgroups per
   // compute unit busy (a second, nearly empty round would double the kernel
-  // time).  A split holds at least two key tiles, at most the paged table's
-  // cap, and the merge kernel's table bounds the number of splits.
+  // time).  That gives the shortest split considered; a split holds at least
+  // two key tiles, at most the paged table's cap, and the merge kernel's
+  // table bounds the number of splits.
   const int64_t units = static_cast<int64_t>(s.B) * s.Hkv * p->row_tiles;
   const int64_t target = static_cast<int64_t>(kWgsPerCu) * num_cus;
   const int64_t want = std::max<int64_t>(1, target / units);
-  int64_t sk = (s.max_prefix + want - 1) / want;
-  sk = std::max<int64_t>(sk, (s.max_prefix + kMaxMergeSplits - 1) / kMaxMergeSplits);
-  sk = std::max<int64_t>((sk + kKT - 1) / kKT * kKT, 2 * kKT);
-  sk = std::min<int64_t>(sk, static_cast<int64_t>(kMaxSplitTiles) * kKT);
-  sk = std::min(sk, split_key_cap(s));
-  p->split_keys = static_cast<int>(sk);
-  p->max_splits = static_cast<int>(std::max<int64_t>(1, (s.max_prefix + sk - 1) / sk));
-  // Partials exist only when some sequence can have more than one split.
+  const int64_t mp = s.max_prefix;
+  const int64_t cap = std::min(split_key_cap(s), static_cast<int64_t>(kMaxSplitTiles) * kKT);
+  int64_t sk0 = (mp + want - 1) / want;
+  sk0 = std::max<int64_t>(sk0, (mp + kMaxMergeSplits - 1) / kMaxMergeSplits);
+  sk0 = std::max<int64_t>((sk0 + kKT - 1) / kKT * kKT, 2 * kKT);
+  sk0 = std::min(sk0, cap);
+  // From there up to the cap, the split length (and whether the tree takes a
+  // split of its own) with the lowest estimated time: this balances the
+  // split that carries the tree against the others.
+  int64_t best_sk = sk0;
+  bool best_alone = false;
+  double best = plan_cost(mp, s.Nmax, sk0, false, units, target);
+  for (int64_t sk = sk0; sk <= cap; sk += kKT) {
+    for (int alone = 0; alone < 2; ++alone) {
+      if (alone && n_splits_of(static_cast<int>(mp), s.Nmax, static_cast<int>(sk), 1) >
+                       kMaxMergeSplits)
+        continue;
+      const double c = plan_cost(mp, s.Nmax, sk, alone != 0, units, target);
+      if (c < best) {
+        best = c;
+        best_sk = sk;
+        best_alone = alone != 0;
+      }
+    }
+  }
+  p->split_keys = static_cast<int>(best_sk);
+  p->tree_alone = best_alone;
+  p->max_splits = n_splits_of(static_cast<int>(mp), s.Nmax, p->split_keys, best_alone);
+  // Workspace for partials, sized from the shortest split considered (the
+  // most splits any plan of this shape can have), so that a layout with a
+  // smaller cap never needs more than the size reported for the worst one.
+  // None when no sequence can have more than one split.
+  const int64_t pre0 = (mp + sk0 - 1) / sk0;
+  const int64_t bound = pre0 <= 1 ? 1 : std::min<int64_t>(pre0 + 1, kMaxMergeSplits);
   const int64_t Mpad = static_cast<int64_t>(p->row_tiles) * kTileRows;
-  const int64_t slots = static_cast<int64_t>(s.B) * s.Hkv * p->max_splits * Mpad;
+  const int64_t slots = static_cast<int64_t>(s.B) * s.Hkv * bound * Mpad;
   p->workspace_bytes =
-      p->max_splits > 1 ? static_cast<size_t>(slots) * (kD * sizeof(uint16_t) + 2 * sizeof(float)) : 0;
+      bound > 1 ? static_cast<size_t>(slots) * (kD * sizeof(uint16_t) + 2 * sizeof(float)) : 0;
   p->mfma = true;
 }
 
@@ -834,6 +934,7 @@ hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q
   a.Mpad = static_cast<int>(Mpad);
   a.split_keys = p.split_keys;
   a.max_splits = p.max_splits;
+  a.tree_alone = p.tree_alone ? 1 : 0;
   a.scale_log2 = scale * kLog2e;
   const dim3 grid(s.B * s.Hkv, p.row_tiles, p.max_splits);
   hipLaunchKernelGGL(attn_mfma_kernel, grid, dim3(kThreads), 0, stream, a);

@@ -26,11 +26,14 @@ struct AttnPlan {
   int row_tiles;   // workgroups along the stacked rows
   int tile_rows;   // rows per workgroup
   int split_keys;  // prefix keys per split (multiple of the key tile)
-  int max_splits;  // KV splits for max_prefix (the last also takes the tree keys)
+  int max_splits;  // KV splits of the longest sequence (max_prefix keys, Nmax nodes)
+  bool tree_alone; // the tree's keys may take a split of their own
   bool mfma;       // bf16 MFMA split-KV path (else the row-wise VALU path)
   size_t workspace_bytes;
 };
 AttnPlan plan_attention(const AttnShape& s, int num_cus);
+// KV splits of a sequence with `prefix` keys and `n` tree nodes under a plan.
+int attention_splits(const AttnPlan& p, int prefix, int n);
 hipError_t launch_attention(const AttnShape& s, const AttnPlan& plan, const void* q,
                             const void* k_cache, const void* v_cache, const int32_t* block_table,
                             const int32_t* prefix_len, const int32_t* parents,

@@ -35,7 +35,8 @@ def test_version_and_workspace_queries():
     assert ltd.accept_workspace_size(1, 60, 128256) == 1 * 60 * 16 * 8
     assert ltd.accept_workspace_size(1, 300, 10) == 0  # Nmax above the node limit
     assert ltd.attn_workspace_size(1, 60, 32, 8, 96, 2048, ltd.DTYPE_BF16) == 0  # unsupported d
-    assert ltd.attn_num_splits(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 4096) == -1
+    assert ltd.attn_num_splits(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 4096, 60) == -1
+    assert ltd.attn_num_splits(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 2048, 61) == -1
 
 
 def test_library_links_only_hip_runtime():
@@ -68,14 +69,20 @@ def test_bf16_head128_workloads_plan_the_mfma_split_path():
     16-sequence 70B-shaped batch already has more units than compute units;
     its splits are only capped at 32 key tiles (2048 keys) so that no single
     workgroup's chain of tiles dominates, and a sequence that fits one split
-    is written without a merge pass.  The workspace size covers the paged
+    is written without a merge pass.  Where compute units are left over, the
+    tree's keys get a split of their own.  The workspace size covers the paged
     layout with the most splits.  fp32 and d=64 run on the row-wise kernel."""
     for B, Nmax, Hq, Hkv, P in ((1, 60, 32, 8, 2048), (1, 60, 32, 8, 16384), (1, 256, 64, 8, 4096)):
-        assert ltd.attn_num_splits(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16, P) > 1
+        assert ltd.attn_num_splits(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16, P, Nmax) > 1
         assert ltd.attn_workspace_size(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16) > 0
-    assert ltd.attn_num_splits(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16, 8192) == 4
-    assert ltd.attn_num_splits(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16, 2048) == 1
-    assert ltd.attn_num_splits(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16, 0) == 1
+    # 8B shape, prefix 2048: 16 two-tile prefix splits and the 60-node tree
+    # in a split of its own (the last prefix split has no room for it)
+    assert ltd.attn_num_splits(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 2048, 60) == 17
+    assert ltd.attn_num_splits(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 2048, 0) == 16
+    assert ltd.attn_num_splits(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 100, 60) == 1
+    assert ltd.attn_num_splits(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16, 8192, 128) == 4
+    assert ltd.attn_num_splits(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16, 2048, 128) == 1
+    assert ltd.attn_num_splits(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16, 0, 128) == 1
     assert ltd.attn_workspace_size(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16) > 0
-    assert ltd.attn_num_splits(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32, 128) == 1
+    assert ltd.attn_num_splits(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32, 128, 16) == 1
     assert ltd.attn_workspace_size(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32) == 0

@@ -149,6 +149,20 @@ def test_argmax_ties_signed_zero_and_ragged_vocab():
 
 
 @pytest.mark.parametrize("block_size", [0, 16])
+@pytest.mark.parametrize("P,N,Hq", [(2048, 60, 32), (1999, 60, 32), (2048, 128, 8)])
+def test_tree_keys_in_a_split_of_their_own(P, N, Hq, block_size):
+    """A prefix spanning many short splits whose last one is (nearly) full:
+    the tree's keys take a split of their own (one or two tiles), and with
+    P=1999 the last prefix split ends in a partial tile."""
+    rng = np.random.default_rng(P + N)
+    b = _custom([W.tree_uniform_parent(rng, N)], [P], Hq=Hq, Hkv=8, Nmax=N, block_size=block_size,
+                seed=P + N, label=f"tree split P={P} N={N} block={block_size}")
+    shape = (b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix, b.dtype)
+    assert ltd.attn_num_splits(*shape, P, N) == ltd.attn_num_splits(*shape, P, 0) + 1 > 2
+    _full_step(b)
+
+
+@pytest.mark.parametrize("block_size", [0, 16])
 def test_single_split_batch_writes_output_directly(block_size):
     """A batch whose longest prefix fits one KV split: every (sequence, kv
     head) is one workgroup that also takes the tree keys and writes the output
@@ -162,5 +176,6 @@ def test_single_split_batch_writes_output_directly(block_size):
     b = _custom(trees, prefix, Hq=32, Hkv=4, Nmax=64, block_size=block_size, seed=41,
                 label=f"single-split batch block={block_size}")
     assert ltd.attn_workspace_size(b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix, b.dtype) == 0
-    assert ltd.attn_num_splits(b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix, b.dtype, b.max_prefix) == 1
+    assert ltd.attn_num_splits(b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix, b.dtype, b.max_prefix,
+                               b.Nmax) == 1
     _full_step(b)
