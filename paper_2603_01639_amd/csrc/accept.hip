@@ -9,11 +9,17 @@
 //       (order-preserving value bits << 32) | (0xFFFFFFFF - index)
 //     whose maximum is the largest value with the lowest index; -0.0 is
 //     folded onto +0.0 before packing, so the two compare equal.
-//  2. accept_scan_kernel: one workgroup per sequence, one thread per node.
-//     It finishes the argmax from the chunk keys, then computes acceptance
-//     and depth with pointer doubling over the parent links (log2 N rounds),
-//     picks the deepest accepted node (smallest index on ties), and emits the
-//     path by binary lifting from that leaf.
+//  2. accept_scan_kernel: one workgroup per sequence.  It fetches every chunk
+//     key of the sequence in one round of independent loads spread over all
+//     threads, issued before the node count arrives (they stay inside the
+//     sequence's Nmax * chunks keys), and folds them into per-node maxima in
+//     LDS; then, one thread per node, acceptance and depth by pointer doubling
+//     over the parent links (ceil(log2 N) rounds), the deepest accepted node
+//     (smallest index on ties), and the path by binary lifting from that leaf.
+// The kernel boundary is the only synchronisation between the two: on this
+// chip a device-scope atomic round trip costs about as much as the whole scan,
+// and an agent-scope fence (an L2 write-back) in every argmax workgroup costs
+// several times the argmax.
 #include "ltd_device.hpp"
 #include "ltd_launch.hpp"
 
@@ -21,8 +27,12 @@ namespace ltd {
 namespace {
 
 constexpr int kArgmaxThreads = 256;
-constexpr int kChunk = 8192;  // logits per argmax workgroup (32 KiB)
-constexpr int kLiftLevels = 8;  // 2^8 = LTD_MAX_NODES
+constexpr int kChunk = 8192;                                // logits per workgroup (32 KiB)
+constexpr int kVecPerThread = kChunk / 4 / kArgmaxThreads;  // 16-byte loads per thread
+constexpr int kVecInFlight = 4;  // loads per batch (measured: 4 beats 8 and 2)
+constexpr int kScanThreads = LTD_MAX_NODES;                 // one thread per node
+constexpr int kKeysPerRound = 8;                            // key loads in flight per thread
+constexpr int kLiftLevels = 8;                              // 2^8 = LTD_MAX_NODES
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -35,13 +45,11 @@ __device__ __forceinline__ uint64_t pack_key(float v, int idx) {
 __device__ __forceinline__ int key_index(uint64_t key) {
   return static_cast<int>(0xFFFFFFFFu - static_cast<uint32_t>(key));
 }
+__device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return b > a ? b : a; }
 
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
 #pragma unroll
-  for (int off = kWave / 2; off > 0; off >>= 1) {
-    const uint64_t o = __shfl_xor(v, off, kWave);
-    v = o > v ? o : v;
-  }
+  for (int off = kWave / 2; off > 0; off >>= 1) v = max_u64(v, __shfl_xor(v, off, kWave));
   return v;
 }
 
@@ -57,23 +65,31 @@ __global__ void __launch_bounds__(kArgmaxThreads) argmax_partial_kernel(
   const int hi = min(Voc, lo + kChunk);
   uint64_t best = 0;
   if (kVec4) {
+    // Elements 4f .. 4f+3 of the row for f = lo/4 + tid + 256u.
     const f32x4* row4 = reinterpret_cast<const f32x4*>(row);
-#pragma unroll 4
-    for (int f = (lo >> 2) + threadIdx.x; f < (hi >> 2); f += kArgmaxThreads) {
-      const f32x4 x = __builtin_nontemporal_load(row4 + f);
-      const int v = f << 2;
-      uint64_t k0 = pack_key(x.x, v), k1 = pack_key(x.y, v + 1);
-      uint64_t k2 = pack_key(x.z, v + 2), k3 = pack_key(x.w, v + 3);
-      k0 = k1 > k0 ? k1 : k0;
-      k2 = k3 > k2 ? k3 : k2;
-      k0 = k2 > k0 ? k2 : k0;
-      best = k0 > best ? k0 : best;
+    const int f0 = (lo >> 2) + threadIdx.x;
+    const int fend = hi >> 2;
+#pragma unroll
+    for (int u0 = 0; u0 < kVecPerThread; u0 += kVecInFlight) {
+      f32x4 x[kVecInFlight];
+#pragma unroll
+      for (int u = 0; u < kVecInFlight; ++u) {
+        const int f = f0 + (u0 + u) * kArgmaxThreads;
+        x[u] = f < fend ? __builtin_nontemporal_load(row4 + f) : (f32x4){0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int u = 0; u < kVecInFlight; ++u) {
+        const int f = f0 + (u0 + u) * kArgmaxThreads;
+        if (f < fend) {
+          const int v = f << 2;
+          const uint64_t k01 = max_u64(pack_key(x[u].x, v), pack_key(x[u].y, v + 1));
+          const uint64_t k23 = max_u64(pack_key(x[u].z, v + 2), pack_key(x[u].w, v + 3));
+          best = max_u64(best, max_u64(k01, k23));
+        }
+      }
     }
   } else {
-    for (int v = lo + threadIdx.x; v < hi; v += kArgmaxThreads) {
-      const uint64_t k = pack_key(row[v], v);
-      best = k > best ? k : best;
-    }
+    for (int v = lo + threadIdx.x; v < hi; v += kArgmaxThreads) best = max_u64(best, pack_key(row[v], v));
   }
   __shared__ uint64_t wave_best[kArgmaxThreads / kWave];
   best = wave_max_u64(best);
@@ -81,16 +97,17 @@ __global__ void __launch_bounds__(kArgmaxThreads) argmax_partial_kernel(
   __syncthreads();
   if (threadIdx.x == 0) {
     uint64_t r = wave_best[0];
-    for (int w = 1; w < kArgmaxThreads / kWave; ++w) r = wave_best[w] > r ? wave_best[w] : r;
+    for (int w = 1; w < kArgmaxThreads / kWave; ++w) r = max_u64(r, wave_best[w]);
     partial[(static_cast<int64_t>(b) * Nmax + i) * chunks + chunk] = r;
   }
 }
 
-__global__ void __launch_bounds__(LTD_MAX_NODES) accept_scan_kernel(
+__global__ void __launch_bounds__(kScanThreads) accept_scan_kernel(
     const uint64_t* __restrict__ partial, int chunks, const int32_t* __restrict__ draft_tokens,
     const int32_t* __restrict__ parents, const int32_t* __restrict__ n_nodes, int Nmax,
     int32_t* __restrict__ pred_out, int32_t* __restrict__ accepted_nodes,
     int32_t* __restrict__ out_tokens, int32_t* __restrict__ n_accepted, const int32_t* status) {
+  __shared__ unsigned long long key_s[LTD_MAX_NODES];
   __shared__ int pred_s[LTD_MAX_NODES];
   __shared__ int tok_s[LTD_MAX_NODES];
   __shared__ int16_t up_s[kLiftLevels][LTD_MAX_NODES];  // 2^r-th ancestor, -1 past the root
@@ -101,22 +118,51 @@ __global__ void __launch_bounds__(LTD_MAX_NODES) accept_scan_kernel(
   const int b = blockIdx.x;
   const int c = threadIdx.x;
   if (halted(status)) return;
-  const int n = n_nodes[b];
   const int64_t base = static_cast<int64_t>(b) * Nmax;
-
-  int parent = -1;
+  // Everything the scan reads is requested in one round, before n is known:
+  // the node's token and parent and the first kKeysPerRound * 256 chunk keys
+  // of the sequence (key k = node k / chunks, chunk k % chunks; thread c
+  // takes keys c + 256 j), all inside the sequence's Nmax rows.
+  const int total_max = Nmax * chunks;
+  const uint64_t* pk = partial + base * chunks;
+  const int c_in = min(c, Nmax - 1);
+  const int tok = draft_tokens[base + c_in];
+  const int parent = c == 0 ? -1 : parents[base + c_in];
+  uint64_t key[kKeysPerRound];
+#pragma unroll
+  for (int j = 0; j < kKeysPerRound; ++j) {
+    const int k = j * kScanThreads + c;
+    key[j] = k < total_max ? pk[k] : 0;
+  }
+  const int n = n_nodes[b];
+  key_s[c] = 0;
+  if (c == 0) best_s = 0;
+  __syncthreads();
+  // Fold the keys into per-node maxima with LDS atomics; sequences with more
+  // than kKeysPerRound * 256 keys take further rounds.
+  const int total = n * chunks;
+  for (int k0 = 0; k0 < total; k0 += kKeysPerRound * kScanThreads) {
+    if (k0 > 0) {
+#pragma unroll
+      for (int j = 0; j < kKeysPerRound; ++j) {
+        const int k = k0 + j * kScanThreads + c;
+        key[j] = k < total ? pk[k] : 0;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kKeysPerRound; ++j) {
+      const int k = k0 + j * kScanThreads + c;
+      if (k < total) atomicMax(&key_s[k / chunks], static_cast<unsigned long long>(key[j]));
+    }
+  }
+  __syncthreads();
   if (c < n) {
-    uint64_t key = 0;
-    const uint64_t* pk = partial + (base + c) * chunks;
-    for (int j = 0; j < chunks; ++j) key = pk[j] > key ? pk[j] : key;
-    const int p = key_index(key);
+    const int p = key_index(key_s[c]);
     pred_s[c] = p;
     pred_out[base + c] = p;
-    tok_s[c] = draft_tokens[base + c];
-    parent = parents[base + c];
+    tok_s[c] = tok;
     up_s[0][c] = static_cast<int16_t>(c == 0 ? -1 : parent);
   }
-  if (c == 0) best_s = 0;
   __syncthreads();
 
   // valid(c): the draft token equals the target's prediction at the parent.
@@ -127,7 +173,12 @@ __global__ void __launch_bounds__(LTD_MAX_NODES) accept_scan_kernel(
     dep_s[0][c] = (c == 0) ? 0 : 1;
   }
   __syncthreads();
+  // Round r folds in the 2^r-th ancestor's values and builds level r + 1 of
+  // the ancestor table.  After R rounds each node covers 2^R links of its root
+  // path, so ceil(log2 n) rounds (at least one) cover every depth < n, and the
+  // levels built are those the lifting below needs for steps < n.
   for (int r = 0; r < kLiftLevels; ++r) {
+    if (r > 0 && (1 << r) >= n) break;  // uniform: every thread leaves together
     if (c < n) {
       const int j = up_s[r][c];
       int ok = ok_s[cur][c], dep = dep_s[cur][c];
@@ -151,7 +202,7 @@ __global__ void __launch_bounds__(LTD_MAX_NODES) accept_scan_kernel(
   const int len = (best_s >> 16) + 1;
 
   // Thread k < len writes the path node at depth k: the (len-1-k)-th ancestor
-  // of the leaf, by binary lifting.
+  // of the leaf, by binary lifting (len - 1 < n needs only the levels built).
   if (c < len) {
     int steps = len - 1 - c, j = leaf;
     for (int r = 0; r < kLiftLevels; ++r)
@@ -188,7 +239,7 @@ hipError_t launch_accept(const float* logits, const int32_t* draft_tokens, const
                        logits, n_nodes, Nmax, Voc, chunks, partial, status);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(accept_scan_kernel, dim3(B), dim3(LTD_MAX_NODES), 0, stream, partial, chunks,
+  hipLaunchKernelGGL(accept_scan_kernel, dim3(B), dim3(kScanThreads), 0, stream, partial, chunks,
                      draft_tokens, parents, n_nodes, Nmax, pred, accepted_nodes, out_tokens,
                      n_accepted, status);
   return hipGetLastError();

@@ -716,11 +716,16 @@ __global__ void __launch_bounds__(kThreads, 1) attn_mfma_kernel(MfmaArgs a) {
 // One wave per stacked row: combine the splits' partials
 //   out = sum_s w_s * Ohat_s / sum_s w_s,  w_s = 2^(m_s - M) * l_s,  M = max_s m_s,
 // where Ohat_s = O_s / l_s is the split's normalised output (bf16).  Lane s
-// first takes split s's (m, l); then the 4 groups of 16 lanes each read one
-// split's row (16 bytes = 8 dims per lane) per step, so 4 splits' rows are in
-// flight per load, and the groups' sums are added with two lane exchanges.
+// takes split s's (m, l); the 4 groups of 16 lanes each read one split's row
+// (16 bytes = 8 dims per lane) per step, so 4 splits' rows are in flight per
+// load, and the groups' sums are added with two lane exchanges.  The kernel
+// is latency-bound, so the (m, l) pairs and the first 16 splits' rows are
+// requested before the sequence's prefix length and node count arrive: every
+// row of the grid is inside the workspace's Mpad rows, and every split index
+// below max_splits inside its splits.
 __global__ void __launch_bounds__(256) attn_merge_kernel(MfmaArgs a) {
   __shared__ float w_s[4][kMaxMergeSplits];
+  constexpr int kFirst = 16;  // splits whose rows are requested up front
   const int bg = blockIdx.x;
   const int b = bg / a.Hkv;
   const int g = bg % a.Hkv;
@@ -728,19 +733,32 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(MfmaArgs a) {
   const int wv = threadIdx.x / kWave;
   const int row = blockIdx.y * 4 + wv;
   const int lane = threadIdx.x % kWave;
+  const int grp = lane >> 4, col = lane & 15;  // split offset, 8-dim chunk
+  const int64_t part0 = static_cast<int64_t>(bg) * a.max_splits * a.Mpad + row;
+  const unsigned char* op = reinterpret_cast<const unsigned char*>(a.ws_o + part0 * kD) + col * 16;
+  const int64_t stride = static_cast<int64_t>(a.Mpad) * kD * 2;  // bytes between splits
+  f32x2 ml0 = {-INFINITY, 0.f};
+  if (lane < a.max_splits) ml0 = *reinterpret_cast<const f32x2*>(a.ws_ml + (part0 + lane * a.Mpad) * 2);
+  u32x4 o0[kFirst / 4];
+#pragma unroll
+  for (int u = 0; u < kFirst / 4; ++u) {
+    const int sp = 4 * u + grp;
+    o0[u] = sp < a.max_splits ? *reinterpret_cast<const u32x4*>(op + sp * stride)
+                              : (u32x4){0u, 0u, 0u, 0u};
+  }
   const int n = a.n_nodes[b];
+  const int P = a.prefix_len[b];
   if (row >= a.G * n) return;
   // (clamped so that a prefix above the planned maximum cannot index past the
   // workspace; such input is malformed and caught when validation is on)
-  const int n_splits = min(n_splits_of(a.prefix_len[b], n, a.split_keys, a.tree_alone), a.max_splits);
+  const int n_splits = min(n_splits_of(P, n, a.split_keys, a.tree_alone), a.max_splits);
   if (n_splits == 1) return;  // the attention kernel wrote this row's output
-  const int64_t part0 = static_cast<int64_t>(bg) * a.max_splits * a.Mpad + row;
-  float M = -INFINITY;
-  for (int s = lane; s < n_splits; s += kWave) M = fmaxf(M, a.ws_ml[(part0 + s * a.Mpad) * 2]);
+  float M = lane < n_splits ? ml0.x : -INFINITY;
+  for (int s = lane + kWave; s < n_splits; s += kWave) M = fmaxf(M, a.ws_ml[(part0 + s * a.Mpad) * 2]);
   M = wave_max(M);
   float wsum = 0.f;
   for (int s = lane; s < n_splits; s += kWave) {
-    const f32x2 ml = *reinterpret_cast<const f32x2*>(a.ws_ml + (part0 + s * a.Mpad) * 2);
+    const f32x2 ml = s == lane ? ml0 : *reinterpret_cast<const f32x2*>(a.ws_ml + (part0 + s * a.Mpad) * 2);
     const float w = exp2_fast(ml.x - M) * ml.y;
     w_s[wv][s] = w;
     wsum += w;
@@ -749,11 +767,20 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(MfmaArgs a) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  const int grp = lane >> 4, col = lane & 15;  // split offset, 8-dim chunk
-  const unsigned char* op = reinterpret_cast<const unsigned char*>(a.ws_o + part0 * kD) + col * 16;
-  const int64_t stride = static_cast<int64_t>(a.Mpad) * kD * 2;  // bytes between splits
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int s0 = 0; s0 < n_splits; s0 += 16) {
+  auto fold = [&](const u32x4& o, float w) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc[2 * e] += w * bf16_to_f32(static_cast<uint16_t>(o[e] & 0xFFFFu));
+      acc[2 * e + 1] += w * bf16_to_f32(static_cast<uint16_t>(o[e] >> 16));
+    }
+  };
+#pragma unroll
+  for (int u = 0; u < kFirst / 4; ++u) {
+    const int sp = 4 * u + grp;
+    if (sp < n_splits) fold(o0[u], w_s[wv][sp]);
+  }
+  for (int s0 = kFirst; s0 < n_splits; s0 += 16) {
     u32x4 o[4];
     float w[4];
 #pragma unroll
@@ -767,12 +794,7 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(MfmaArgs a) {
       }
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc[2 * e] += w[u] * bf16_to_f32(static_cast<uint16_t>(o[u][e] & 0xFFFFu));
-        acc[2 * e + 1] += w[u] * bf16_to_f32(static_cast<uint16_t>(o[u][e] >> 16));
-      }
+    for (int u = 0; u < 4; ++u) fold(o[u], w[u]);
   }
 #pragma unroll
   for (int e = 0; e < 8; ++e) {

@@ -32,24 +32,27 @@ __global__ void __launch_bounds__(kThreads) kv_compact_kernel(
   const int g = (y >> 1) % Hkv;
   const int layer = (y >> 1) / Hkv;
   if (halted(status)) return;
-  const int P = prefix_len[b];
-  const int n = n_accepted[b];
+  // The first pass's path entries are loaded together with P and n (j is
+  // clamped below Nmax, so the load is in bounds whatever n is).
   const int32_t* path = accepted_nodes + static_cast<int64_t>(b) * Nmax;
-  unsigned char* base = (which ? v_cache : k_cache) + layer * layer_stride_bytes;
-
   const int vec_per_row = row_bytes / 16;
   const int rows_per_pass = kThreads / vec_per_row;
   const int rj = threadIdx.x / vec_per_row;
   const int col = threadIdx.x % vec_per_row;
+  int pj = path[min(rj, Nmax - 1)];
+  const int P = prefix_len[b];
+  const int n = n_accepted[b];
+  unsigned char* base = (which ? v_cache : k_cache) + layer * layer_stride_bytes;
+
   for (int j0 = 0; j0 < n; j0 += rows_per_pass) {
     const int j = j0 + rj;
-    const bool active = rj < rows_per_pass && j < n && path[j] != j;
+    if (j0 > 0) pj = path[min(j, Nmax - 1)];
+    const bool active = rj < rows_per_pass && j < n && pj != j;
     u32x4 v = {0, 0, 0, 0};
     int64_t dst = 0;
     if (active) {
       // cache_row counts elements of a `row_bytes`-wide row with d = row_bytes
-      const int64_t src = cache_row(block_table, b, g, P + path[j], Hkv, row_bytes, kv_rows,
-                                    max_blocks);
+      const int64_t src = cache_row(block_table, b, g, P + pj, Hkv, row_bytes, kv_rows, max_blocks);
       dst = cache_row(block_table, b, g, P + j, Hkv, row_bytes, kv_rows, max_blocks);
       v = *reinterpret_cast<const u32x4*>(base + src + col * 16);
     }

@@ -179,3 +179,42 @@ def test_single_split_batch_writes_output_directly(block_size):
     assert ltd.attn_num_splits(b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix, b.dtype, b.max_prefix,
                                b.Nmax) == 1
     _full_step(b)
+
+
+def test_accept_workspace_reused_across_calls():
+    """One acceptance workspace serves a sequence of calls with different B,
+    Nmax and vocabularies, including a call that validation stops: no call
+    depends on what an earlier one left in it."""
+    import torch
+    rng = np.random.default_rng(23)
+    ws = torch.empty(max(ltd.accept_workspace_size(16, 128, 128256),
+                         ltd.accept_workspace_size(3, 256, 9000)), dtype=torch.uint8, device="cuda")
+    batches = [W.config5_paged(0)]
+    for n_list, voc in (((256, 3, 77), 9000), ((60,), 128256), ((5, 200), 8192)):
+        trees = [W.tree_uniform_parent(rng, n) for n in n_list]
+        batches.append(_custom(trees, [0] * len(trees), Hq=2, Hkv=1, d=64, Voc=voc,
+                               seed=len(n_list), label=f"reuse N={n_list} Voc={voc}"))
+    batches.append(W.config2_8b(3))
+    i32 = dict(dtype=torch.int32, device="cuda")
+    for k, b in enumerate(batches):
+        dev = U.upload(b)
+        if k == 2:
+            # validation stops this call: parents[0][5] = 5 is not below 5
+            bad = dev.parents.clone()
+            bad[0, 5] = 5
+            st = torch.full((1,), -1, **i32)
+            outs = [torch.full((b.B, b.Nmax), -1, **i32) for _ in range(3)]
+            ltd.tree_accept(dev.logits, dev.tokens, bad, dev.n_nodes, *outs,
+                            torch.zeros((b.B,), **i32), workspace=ws, validate=True, status=st)
+            torch.cuda.synchronize()
+            assert int(st.item()) == ltd.STATUS_BAD_PARENT and (outs[0] == -1).all()
+        U.log(f"[parity] accept workspace reuse, call {k}: {b.label}")
+        pred = torch.full((b.B, b.Nmax), -1, **i32)
+        acc = torch.full((b.B, b.Nmax), -1, **i32)
+        toks = torch.full((b.B, b.Nmax), -1, **i32)
+        nacc = torch.zeros((b.B,), **i32)
+        ltd.tree_accept(dev.logits, dev.tokens, dev.parents, dev.n_nodes, pred, acc, toks, nacc,
+                        workspace=ws)
+        torch.cuda.synchronize()
+        U.check_accept(b, (pred.cpu().numpy(), acc.cpu().numpy(), toks.cpu().numpy(),
+                           nacc.cpu().numpy()))
