@@ -93,7 +93,8 @@ extern "C" {
  *   parents     [B][Nmax] int32, n_nodes [B] int32 in [1, Nmax].
  *   out         [B][Nmax][Hq][d] (dtype); rows i >= n_nodes[b] are not written.
  *   Hq % Hkv == 0, d in {64, 128}, 1 <= Nmax <= LTD_MAX_NODES.
- *   scale       softmax scale (1/sqrt(d) for standard attention).
+ *   scale       softmax scale, finite and > 0 (1/sqrt(d) for standard
+ *               attention); anything else is LTD_EINVAL.
  *   workspace   device scratch of at least ltd_tree_verify_attn_workspace_size()
  *               bytes for the same (B, Nmax, Hq, Hkv, d, max_prefix, dtype) (that
  *               size covers every cache layout; it is 0 when no sequence can

@@ -2,6 +2,7 @@
 // plans and kernel dispatch.  No allocation, no synchronisation.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <mutex>
 
 #include "ltd_launch.hpp"
@@ -73,6 +74,7 @@ int ltd_tree_verify_attn(const void* q, const void* k_cache, const void* v_cache
                          int num_blocks, float scale, int dtype, void* workspace,
                          size_t workspace_bytes, int validate, int32_t* status, void* stream) {
   if (!attn_args_ok(B, Nmax, Hq, Hkv, d, max_prefix, dtype) || kv_rows < 1) return LTD_EINVAL;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return LTD_EINVAL;
   if (!attn_supported(d, dtype)) return LTD_EUNSUPPORTED;
   if (block_table && (max_blocks < 1 || num_blocks < 1)) return LTD_EINVAL;
   if (validate && !status) return LTD_EINVAL;

@@ -96,6 +96,7 @@ struct MfmaArgs {
   int Nmax, Hq, Hkv, G, kv_rows, max_blocks;
   int Mpad, split_keys, max_splits, tree_alone;
   float scale_log2;
+  float lazy_gap;  // kLazyMax / scale_log2: the raw-score margin of the lazy max
 };
 
 // A-row i of a 32-key block reads key sigma(i); accumulator register r of lane
@@ -514,24 +515,28 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
       for (int r = 0; r < 16; r += 2)
         tmax = __builtin_elementwise_maximum(tmax, __builtin_elementwise_maximum(s[kb][r], s[kb][r + 1]));
     tmax = __builtin_elementwise_maximum(tmax, xor32(tmax));
-    m_new = (tmax * c > m_run * c + kLazyMax || m_run == -INFINITY) ? fmaxf(m_run, tmax) : m_run;
+    // (scale > 0, so the lazy test can run on raw scores)
+    m_new = tmax > m_run + a.lazy_gap ? tmax : m_run;
     const float neg = (m_new == -INFINITY) ? 0.f : -m_new * c;
+    // The row sum adds the rounded bf16 probabilities, two per
+    // v_dot2_f32_bf16 with ones: the very weights P.V multiplies.
+    const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
     float ps = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        float p[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          p[j] = exp2_fast(__builtin_fmaf(s[kb][8 * kk + j], c, neg));
-          ps += p[j];
-        }
         u32x4 pk;
-        pk.x = pack_bf16x2(p[0], p[1]);
-        pk.y = pack_bf16x2(p[2], p[3]);
-        pk.z = pack_bf16x2(p[4], p[5]);
-        pk.w = pack_bf16x2(p[6], p[7]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float p0 = exp2_fast(__builtin_fmaf(s[kb][8 * kk + 2 * j], c, neg));
+          const float p1 = exp2_fast(__builtin_fmaf(s[kb][8 * kk + 2 * j + 1], c, neg));
+          // (summed before it goes into the vector: hipcc folds a bf16x2
+          // bit-cast of element j of a u32x4 to element 0)
+          const bf16x2 w = __builtin_convertvector((f32x2){p0, p1}, bf16x2);
+          ps = __builtin_amdgcn_fdot2_f32_bf16(w, ones, ps, false);
+          pk[j] = __builtin_bit_cast(uint32_t, w);
+        }
         pf[kb][kk] = __builtin_bit_cast(bf16x8, pk);
       }
     }
@@ -583,34 +588,42 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     barrier_only();  // tile t landed for all waves; every wave is done with tile t-2
     if (t + kAhead < n_tiles) issue_tile(t + kAhead);
   };
+  // The P^T fragments alternate between two register sets (the loop is
+  // unrolled by two), so tile t-1's are never copied.
   f32x16 s_acc[2];
-  bf16x8 pf[2][2], pf_prev[2][2];
+  bf16x8 pfa[2][2], pfb[2][2];
+  auto body = [&](int t, const bf16x8(&pf_prev)[2][2], bf16x8(&pf)[2][2]) {
+    publish(t);
+    if (active) {
+      load_k(t);
+      scores(s_acc);
+      mask_scores(t, s_acc);
+      accumulate(t - 1, pf_prev);  // tile t-1's P.V ...
+      exponentials(s_acc, pf);     // ... interleaved with tile t's softmax
+      finish_softmax();            // after P.V(t-1): may rescale O
+    }
+  };
   if (n_tiles > 0) {
     publish(0);
     if (active) {
       load_k(0);
       scores(s_acc);
       mask_scores(0, s_acc);
-      exponentials(s_acc, pf);
+      exponentials(s_acc, pfa);
       finish_softmax();
     }
   }
-  for (int t = 1; t < n_tiles; ++t) {
-    publish(t);
-    if (active) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) pf_prev[kb][kk] = pf[kb][kk];
-      load_k(t);
-      scores(s_acc);
-      mask_scores(t, s_acc);
-      accumulate(t - 1, pf_prev);   // tile t-1's P.V ...
-      exponentials(s_acc, pf);      // ... interleaved with tile t's softmax
-      finish_softmax();             // after P.V(t-1): may rescale O
-    }
+  int t = 1;
+  for (; t + 1 < n_tiles; t += 2) {
+    body(t, pfa, pfb);
+    body(t + 1, pfb, pfa);
   }
-  if (n_tiles > 0 && active) accumulate(n_tiles - 1, pf);
+  if (t < n_tiles) {
+    body(t, pfa, pfb);
+    if (active) accumulate(n_tiles - 1, pfb);
+  } else if (n_tiles > 0 && active) {
+    accumulate(n_tiles - 1, pfa);
+  }
 
   // ---- results.  With one split the normalised output O / l goes straight
   // to `out`.  Otherwise the split's partial result: (max in log2 units, sum)
@@ -958,6 +971,7 @@ hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q
   a.max_splits = p.max_splits;
   a.tree_alone = p.tree_alone ? 1 : 0;
   a.scale_log2 = scale * kLog2e;
+  a.lazy_gap = kLazyMax / a.scale_log2;
   const dim3 grid(s.B * s.Hkv, p.row_tiles, p.max_splits);
   hipLaunchKernelGGL(attn_mfma_kernel, grid, dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();

@@ -86,3 +86,14 @@ def test_bf16_head128_workloads_plan_the_mfma_split_path():
     assert ltd.attn_workspace_size(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16) > 0
     assert ltd.attn_num_splits(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32, 128, 16) == 1
     assert ltd.attn_workspace_size(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32) == 0
+
+
+@pytest.mark.parametrize("scale", [0.0, -0.125, float("nan"), float("inf")])
+def test_attention_rejects_a_scale_that_is_not_positive_and_finite(scale):
+    """The softmax scale must be finite and > 0; anything else is refused on
+    the host before any pointer is touched or kernel launched (the pointers
+    here are dummies)."""
+    P = 0x1000  # never dereferenced: the call returns before using them
+    rc = ltd.lib().ltd_tree_verify_attn(P, P, P, None, P, P, P, P, 1, 4, 8, 2, 128, 64, 128, 0, 0,
+                                        scale, ltd.DTYPE_BF16, None, 0, 0, None, None)
+    assert rc == ltd.LTD_EINVAL
