@@ -28,6 +28,7 @@ STATUS_BAD_PARENT = 2
 STATUS_BAD_PREFIX = 3
 STATUS_BAD_BLOCK = 4
 STATUS_BAD_PATH = 5
+STATUS_BAD_SCORE = 6
 
 
 class OracleError(RuntimeError):
@@ -52,6 +53,8 @@ def load_library(path: str) -> ctypes.CDLL:
     lib.ltd_oracle_kv_compact.argtypes = [P, P, P, P, P, P, P, i32, i32, i32, i32, i32, i32,
                                           i32, i32, ctypes.c_int64, i32]
     lib.ltd_oracle_kv_compact.restype = i32
+    lib.ltd_oracle_select_candidates.argtypes = [P, P, P, P, P, i32, i32, i32, P, P, P, P, P]
+    lib.ltd_oracle_select_candidates.restype = i32
     lib.ltd_oracle_num_threads.argtypes = []
     lib.ltd_oracle_num_threads.restype = i32
     return lib
@@ -168,3 +171,24 @@ def kv_compact(k_cache, v_cache, prefix_len, accepted_nodes, n_accepted, *, Hkv,
     if rc != 0:
         raise OracleError(rc)
     return new_len
+
+
+def select_candidates(scores, pool_parents, pool_tokens, pool_size, n_select, Nmax):
+    """Candidate token selection (section 3.2): the V = min(n_select, pool
+    size) candidates of highest cumulative score, flattened in (depth, score,
+    pool index) order.  Returns (selected, parents, tokens, depth, n_nodes);
+    entries past V hold -1."""
+    scores = np.ascontiguousarray(scores, np.float32)
+    B, Vpool = scores.shape
+    pool_parents = np.ascontiguousarray(pool_parents, np.int32)
+    pool_tokens = np.ascontiguousarray(pool_tokens, np.int32)
+    pool_size = np.ascontiguousarray(pool_size, np.int32)
+    n_select = np.ascontiguousarray(n_select, np.int32)
+    outs = [np.full((B, Nmax), -1, np.int32) for _ in range(4)]
+    n_nodes = np.zeros(B, np.int32)
+    rc = _load().ltd_oracle_select_candidates(
+        _ptr(scores), _ptr(pool_parents), _ptr(pool_tokens), _ptr(pool_size), _ptr(n_select),
+        B, Vpool, Nmax, *[_ptr(o) for o in outs], _ptr(n_nodes))
+    if rc != 0:
+        raise OracleError(rc)
+    return (*outs, n_nodes)

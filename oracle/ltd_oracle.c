@@ -20,6 +20,9 @@
  *                    (the bonus token) is appended.
  *   compaction       the rejected candidates are discarded (same paragraph);
  *                    the accepted rows are moved next to the prefix.
+ *   selection        paper section 3.2 ("Candidate Token Selection"): of the
+ *                    draft tree's candidates, the V with the highest predicted
+ *                    (cumulative path) probability are kept and flattened.
  *
  * Readings of points the paper leaves open (softmax scale, node order, whether
  * V counts the root, tie rules, where tree K/V live) are fixed by the caller's
@@ -332,5 +335,99 @@ int ltd_oracle_kv_compact(void* k_cache, void* v_cache, const int32_t* block_tab
     new_prefix_len[b] = P + n;
   }
   free(tmp);
+  return 0;
+}
+
+/* ---- candidate token selection (section 3.2, "Candidate Token Selection").
+ * The paper keeps the V candidates of the draft tree with the highest overall
+ * (cumulative path) probability.  Readings of what it leaves open: equal
+ * scores are ranked by depth, then pool index (a parent never ranks below its
+ * child, since its score is not lower and its depth is), which keeps the kept
+ * set a rooted subtree; the flattened order is by depth, then score, then
+ * pool index, which puts every parent before its children. */
+typedef struct {
+  float score;
+  int depth;
+  int index;
+} cand_t;
+
+static int by_rank(const void* pa, const void* pb) {
+  const cand_t* a = (const cand_t*)pa;
+  const cand_t* b = (const cand_t*)pb;
+  if (a->score != b->score) return a->score > b->score ? -1 : 1;
+  if (a->depth != b->depth) return a->depth < b->depth ? -1 : 1;
+  return (a->index > b->index) - (a->index < b->index);
+}
+
+static int by_flat_order(const void* pa, const void* pb) {
+  const cand_t* a = (const cand_t*)pa;
+  const cand_t* b = (const cand_t*)pb;
+  if (a->depth != b->depth) return a->depth < b->depth ? -1 : 1;
+  if (a->score != b->score) return a->score > b->score ? -1 : 1;
+  return (a->index > b->index) - (a->index < b->index);
+}
+
+int ltd_oracle_select_candidates(const float* scores, const int32_t* pool_parents,
+                                 const int32_t* pool_tokens, const int32_t* pool_size,
+                                 const int32_t* n_select, int B, int Vpool, int Nmax,
+                                 int32_t* selected, int32_t* parents, int32_t* tokens,
+                                 int32_t* depth, int32_t* n_nodes) {
+  if (B < 0 || Vpool < 1 || Nmax < 1) return LTDO_EINVAL;
+  /* data checks first, for every sequence, so nothing is written on failure */
+  for (int b = 0; b < B; ++b) {
+    const int pn = pool_size[b];
+    if (pn < 1 || pn > Vpool || n_select[b] < 1 || n_select[b] > Nmax)
+      return LTDO_STATUS_BAD_NNODES;
+    const int32_t* par = pool_parents + (int64_t)b * Vpool;
+    const float* sc = scores + (int64_t)b * Vpool;
+    if (par[0] != -1) return LTDO_STATUS_BAD_PARENT;
+    for (int i = 1; i < pn; ++i)
+      if (par[i] < 0 || par[i] >= i) return LTDO_STATUS_BAD_PARENT;
+    for (int i = 0; i < pn; ++i) {
+      if (isnan(sc[i])) return LTDO_STATUS_BAD_SCORE;
+      if (i > 0 && sc[i] > sc[par[i]]) return LTDO_STATUS_BAD_SCORE;
+    }
+  }
+  cand_t* c = (cand_t*)malloc(sizeof(cand_t) * (size_t)Vpool);
+  int* dep = (int*)malloc(sizeof(int) * (size_t)Vpool);
+  int* new_id = (int*)malloc(sizeof(int) * (size_t)Vpool);
+  if (!c || !dep || !new_id) {
+    free(c);
+    free(dep);
+    free(new_id);
+    return LTDO_EINVAL;
+  }
+  for (int b = 0; b < B; ++b) {
+    const int pn = pool_size[b];
+    const int32_t* par = pool_parents + (int64_t)b * Vpool;
+    const float* sc = scores + (int64_t)b * Vpool;
+    /* depth: the root is 0, a child one more than its parent (parents come
+     * first in the pool) */
+    for (int i = 0; i < pn; ++i) dep[i] = i == 0 ? 0 : dep[par[i]] + 1;
+    for (int i = 0; i < pn; ++i) {
+      c[i].score = sc[i];
+      c[i].depth = dep[i];
+      c[i].index = i;
+    }
+    /* the V candidates ranked first */
+    qsort(c, (size_t)pn, sizeof(cand_t), by_rank);
+    const int V = n_select[b] < pn ? n_select[b] : pn;
+    /* flattened: depth, then score, then pool index */
+    qsort(c, (size_t)V, sizeof(cand_t), by_flat_order);
+    for (int i = 0; i < pn; ++i) new_id[i] = -1;
+    for (int k = 0; k < V; ++k) new_id[c[k].index] = k;
+    const int64_t o = (int64_t)b * Nmax;
+    for (int k = 0; k < V; ++k) {
+      const int j = c[k].index;
+      selected[o + k] = j;
+      parents[o + k] = j == 0 ? -1 : new_id[par[j]];
+      tokens[o + k] = pool_tokens[(int64_t)b * Vpool + j];
+      depth[o + k] = c[k].depth;
+    }
+    n_nodes[b] = V;
+  }
+  free(c);
+  free(dep);
+  free(new_id);
   return 0;
 }

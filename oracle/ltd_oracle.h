@@ -39,6 +39,7 @@ extern "C" {
 #define LTDO_STATUS_BAD_PREFIX 3
 #define LTDO_STATUS_BAD_BLOCK 4
 #define LTDO_STATUS_BAD_PATH 5
+#define LTDO_STATUS_BAD_SCORE 6
 
 /* Tree attention (paper section 3.2: candidates flattened with a tree
  * attention mask, verified in one target pass).  Node i of sequence b attends
@@ -66,6 +67,22 @@ int ltd_oracle_kv_compact(void* k_cache, void* v_cache, const int32_t* block_tab
                           const int32_t* accepted_nodes, const int32_t* n_accepted, int B,
                           int Nmax, int Hkv, int d, int kv_rows, int max_blocks, int num_blocks,
                           int num_layers, int64_t layer_stride_elems, int elem_bytes);
+
+/* Candidate token selection (paper section 3.2, "Candidate Token
+ * Selection"): from a draft tree of pool_size[b] candidates (pool_parents
+ * [B][Vpool], pool_parents[b][0] = -1 and 0 <= pool_parents[b][i] < i; a
+ * cumulative score per candidate, larger = more probable, never above its
+ * parent's), keep the V = min(n_select[b], pool_size[b]) candidates ranked
+ * first by (score descending, depth ascending, pool index ascending), and
+ * flatten them in (depth ascending, score descending, pool index ascending)
+ * order.  Outputs [B][Nmax] (entries past V untouched): selected = pool
+ * index of node k, parents in the new order (-1 for the root), tokens, depth;
+ * n_nodes[b] = V. */
+int ltd_oracle_select_candidates(const float* scores, const int32_t* pool_parents,
+                                 const int32_t* pool_tokens, const int32_t* pool_size,
+                                 const int32_t* n_select, int B, int Vpool, int Nmax,
+                                 int32_t* selected, int32_t* parents, int32_t* tokens,
+                                 int32_t* depth, int32_t* n_nodes);
 
 /* Threads the oracle's parallel loops use (OpenMP), for reporting. */
 int ltd_oracle_num_threads(void);

@@ -1,10 +1,12 @@
 """Seeded synthetic inputs shaped like the paper's verification workloads.
 
-This module only *draws data*: draft trees, tokens, queries, KV caches, target
-logits and paged block tables.  It contains none of the verification step's
-arithmetic (no attention, no argmax, no acceptance walk, no compaction), so the
-GPU path and the CPU oracle can both consume its arrays without sharing any of
-the method's code.
+This module only *draws data*: draft pools and trees, tokens, queries, KV
+caches, target logits and paged block tables.  It contains none of the
+verification step's arithmetic (no attention, no argmax, no acceptance walk, no
+compaction), so the GPU path and the CPU oracle can both consume its arrays
+without sharing any of the method's code.  Trees for the verification inputs
+are cut from a draft pool by a short selection of the generator's own
+(``tree_eagle``); neither the GPU selection kernel nor the oracle uses it.
 
 Shapes follow the paper's setting (arXiv 2603.01639): Eagle-style beam trees of
 width W and depth D (section 3.2, "Draft Tree Generation"), a verification size
@@ -103,6 +105,16 @@ class DraftTree:
     scores: np.ndarray  # float64 [N] cumulative log-probability (root = 0)
 
 
+@dataclasses.dataclass
+class DraftPool:
+    """Every candidate a beam-like drafter produced, in the order it produced
+    them (the root, then level after level), before any selection."""
+    parents: np.ndarray  # int32 [n]; parents[0] = -1, 0 <= parents[i] < i
+    tokens: np.ndarray  # int32 [n]
+    scores: np.ndarray  # float64 [n] cumulative log-probability (root = 0)
+    level: np.ndarray  # int32 [n] depth below the root
+
+
 def _children_of(parents: np.ndarray) -> List[List[int]]:
     ch: List[List[int]] = [[] for _ in range(len(parents))]
     for i in range(1, len(parents)):
@@ -110,18 +122,22 @@ def _children_of(parents: np.ndarray) -> List[List[int]]:
     return ch
 
 
-def tree_eagle(rng: np.random.Generator, n: int, depth: int, width: int, vocab: int) -> DraftTree:
-    """Beam-like draft tree (section 3.2, "Draft Tree Generation") reranked to
-    the top-``n`` candidates by cumulative score ("Candidate Token Selection").
+def pool_size(depth: int, width: int) -> int:
+    """Candidates in a depth-``depth`` pool: 1 + W + (D-2) W^2 for D >= 2
+    (section 3.2, "Draft Tree Generation"), the root alone for D = 1."""
+    return 1 if depth <= 1 else 1 + width + (depth - 2) * width * width
+
+
+def draft_pool(rng: np.random.Generator, depth: int, width: int, vocab: int) -> DraftPool:
+    """Beam-like draft pool (section 3.2, "Draft Tree Generation").
 
     ``depth`` counts levels including the root: level 1 is the root's top-W
     children, then depth-2 rounds each add the W*W children of the current W
     leaves and keep the top-W of them (by cumulative score) as the next leaves,
     so the pool has 1 + W + (depth-2) * W^2 nodes.  Conditional log-probs of a
     node's W children are the logs of the sorted top-W components of a
-    Dirichlet(0.5 * 1_{W+1}) draw; sibling tokens are distinct.  The top-n set
-    is ancestor-closed because scores strictly decrease along a path; the
-    result is re-indexed by (level, score rank).
+    Dirichlet(0.5 * 1_{W+1}) draw; sibling tokens are distinct.  Scores
+    strictly decrease along every root path.
     """
     pool_par = [-1]
     pool_lvl = [0]
@@ -149,20 +165,31 @@ def tree_eagle(rng: np.random.Generator, n: int, depth: int, width: int, vocab: 
                 cand.extend(expand(leaf))
             cand.sort(key=lambda j: -pool_score[j])
             leaves = cand[:width]
-    total = len(pool_par)
+    return DraftPool(np.array(pool_par, np.int32), np.array(pool_tok, np.int32),
+                     np.array(pool_score, np.float64), np.array(pool_lvl, np.int32))
+
+
+def tree_eagle(rng: np.random.Generator, n: int, depth: int, width: int, vocab: int) -> DraftTree:
+    """A ``draft_pool`` cut down to its top-``n`` candidates by cumulative
+    score (section 3.2, "Candidate Token Selection") and re-indexed by (level,
+    score rank).  The top-n set is ancestor-closed because scores strictly
+    decrease along a path.  (This is the generator's own short selection, used
+    to shape verification inputs; the selection step itself is a separate
+    kernel with its own oracle.)
+    """
+    pool = draft_pool(rng, depth, width, vocab)
+    total = len(pool.parents)
     if n > total:
         raise ValueError(f"tree pool has {total} nodes, asked for {n}")
-    order = sorted(range(total), key=lambda j: -pool_score[j])[:n]
+    order = sorted(range(total), key=lambda j: -pool.scores[j])[:n]
     keep = set(order)
     for j in order:  # ancestor closure (guaranteed by strictly decreasing scores)
-        assert pool_par[j] == -1 or pool_par[j] in keep
-    # re-index by (level, score rank)
-    order.sort(key=lambda j: (pool_lvl[j], -pool_score[j]))
+        assert pool.parents[j] == -1 or pool.parents[j] in keep
+    order.sort(key=lambda j: (pool.level[j], -pool.scores[j]))
     new_id = {old: new for new, old in enumerate(order)}
-    parents = np.array([-1 if pool_par[j] == -1 else new_id[pool_par[j]] for j in order], np.int32)
-    tokens = np.array([pool_tok[j] for j in order], np.int32)
-    scores = np.array([pool_score[j] for j in order], np.float64)
-    return DraftTree(parents, tokens, scores)
+    parents = np.array([-1 if pool.parents[j] == -1 else new_id[pool.parents[j]] for j in order],
+                       np.int32)
+    return DraftTree(parents, pool.tokens[order].astype(np.int32), pool.scores[order].copy())
 
 
 def distinct_sibling_tokens(rng: np.random.Generator, parents: np.ndarray, vocab: int) -> np.ndarray:
@@ -360,3 +387,78 @@ def config5_paged(rep: int = 0, with_logits: bool = True, B: int = 16) -> Verify
     return make_batch(rng, dtype=DTYPE_BF16, Hq=64, Hkv=8, d=128, prefix=prefix, trees=trees,
                       tokens=toks, Voc=128256, p_match=0.7, Nmax=max(ns), block_size=16,
                       with_logits=with_logits, label="70B bf16 paged B16")
+
+
+# ------------------------------------------------------ candidate selection
+
+MAX_POOL = 1024  # candidate pools up to 1 + W + (D-2) W^2 = 1011 (W = 10, D = 12)
+
+
+@dataclasses.dataclass
+class SelectBatch:
+    """Inputs of candidate selection for B sequences: draft pools padded to
+    Vpool columns, and the verification size V each sequence asks for."""
+    B: int
+    Vpool: int
+    Nmax: int
+    scores: np.ndarray  # float32 [B, Vpool] cumulative log-probability
+    pool_parents: np.ndarray  # int32 [B, Vpool]
+    pool_tokens: np.ndarray  # int32 [B, Vpool]
+    pool_size: np.ndarray  # int32 [B]
+    n_select: np.ndarray  # int32 [B]
+    label: str = ""
+
+
+def make_select_batch(pools: List[DraftPool], n_select: List[int], *, Vpool: Optional[int] = None, Nmax: Optional[int] = None,
+                      label: str = "") -> SelectBatch:
+    """Pack pools into [B, Vpool] arrays.  Columns past a pool's size hold
+    junk that a correct consumer never reads (scores above the root's, parent
+    indices out of range, negative tokens)."""
+    B = len(pools)
+    sizes = [len(p.parents) for p in pools]
+    Vpool = Vpool or max(sizes)
+    Nmax = Nmax or max(n_select)
+    scores = np.full((B, Vpool), 1e30, np.float32)
+    par = np.full((B, Vpool), Vpool + 7, np.int32)
+    tok = np.full((B, Vpool), -5, np.int32)
+    for b, p in enumerate(pools):
+        n = sizes[b]
+        # float32 rounding is monotone, so a child never scores above its parent
+        scores[b, :n] = p.scores.astype(np.float32)
+        par[b, :n] = p.parents
+        tok[b, :n] = p.tokens
+    return SelectBatch(B, Vpool, Nmax, scores, par, tok, np.array(sizes, np.int32),
+                       np.array(n_select, np.int32), label)
+
+
+def select_size_action(a: int) -> int:
+    """Verification size of size-policy action a in 0..11: 12 actions mapped
+    linearly onto [20, 240] (appendix A.2, "Size Policy")."""
+    return 20 + 20 * a
+
+
+def select_8b(rep: int = 0) -> SelectBatch:
+    """The 8B-shaped step's selection: one depth-6, width-10 pool (411
+    candidates) cut to V = 60."""
+    rng = rng_for(config_seed(6, rep))
+    pool = draft_pool(rng, 6, 10, 128256)
+    return make_select_batch([pool], [60], label="select D6 W10 pool411 V60")
+
+
+def select_deep(rep: int = 0) -> SelectBatch:
+    """The largest pool: depth 12, width 10 (1011 candidates) cut to V = 240."""
+    rng = rng_for(config_seed(7, rep))
+    pool = draft_pool(rng, 12, 10, 128256)
+    return make_select_batch([pool], [240], Nmax=256, label="select D12 W10 pool1011 V240")
+
+
+def select_batch16(rep: int = 0) -> SelectBatch:
+    """16 sequences with depth uniform in [1, 12] (the depth range the size
+    policy is trained over, section 4, "Initial Policy Training") and V from a uniform size-policy action, padded to 1024
+    pool columns and 256 output rows."""
+    rng = rng_for(config_seed(8, rep))
+    depths = [int(rng.integers(1, 13)) for _ in range(16)]
+    vs = [select_size_action(int(rng.integers(0, 12))) for _ in range(16)]
+    pools = [draft_pool(rng, D, 10, 128256) for D in depths]
+    return make_select_batch(pools, vs, Vpool=MAX_POOL, Nmax=256,
+                             label="select B16 D1-12 W10 V20-240")

@@ -11,6 +11,7 @@ import oracle
 import test_oracle_accept as TA
 import test_oracle_attention as TT
 import test_oracle_compact as TC
+import test_oracle_select as TS
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "ltd_oracle.c")
 
@@ -32,6 +33,13 @@ COMPACT_PINS = [
     lambda: TC.test_contiguous_matches_explicit_gather([0, 4, 5, 9, 11]),
     lambda: TC.test_attention_after_compaction_equals_attention_over_path(),
     lambda: TC.test_paged_multilayer_bf16_moves_the_same_rows(),
+]
+SELECT_PINS = [
+    lambda: TS.test_worked_examples(),
+    lambda: TS.test_exhaustive_small_pools(4),
+    lambda: TS.test_matches_the_generators_own_selection(6, 10, 60),
+    lambda: TS.test_star_pool_is_a_stable_argsort(),
+    lambda: TS.test_validation_codes(),
 ]
 
 # (name, original text, mutated text, pins expected to notice)
@@ -77,6 +85,29 @@ MUTANTS = [
      COMPACT_PINS),
     ("compaction shifts by one row", "int64_t off = cache_row_offset(block_table, b, g, P + j, Hkv",
      "int64_t off = cache_row_offset(block_table, b, g, P + j + 1, Hkv", COMPACT_PINS),
+    ("selection ties ignore depth",
+     "if (a->depth != b->depth) return a->depth < b->depth ? -1 : 1;\n  return (a->index > b->index)",
+     "return (a->index > b->index)", SELECT_PINS),
+    ("selection keeps the lowest scores",
+     "if (a->score != b->score) return a->score > b->score ? -1 : 1;\n  if (a->depth",
+     "if (a->score != b->score) return a->score < b->score ? -1 : 1;\n  if (a->depth", SELECT_PINS),
+    ("flattened order ignores depth",
+     "if (a->depth != b->depth) return a->depth < b->depth ? -1 : 1;\n  if (a->score",
+     "if (a->score", SELECT_PINS),
+    ("flattened order ignores score",
+     "  if (a->score != b->score) return a->score > b->score ? -1 : 1;\n"
+     "  return (a->index > b->index) - (a->index < b->index);\n}\n\nint ltd_oracle_select",
+     "  return (a->index > b->index) - (a->index < b->index);\n}\n\nint ltd_oracle_select",
+     SELECT_PINS),
+    ("parents left as pool indices", "parents[o + k] = j == 0 ? -1 : new_id[par[j]];",
+     "parents[o + k] = j == 0 ? -1 : par[j];", SELECT_PINS),
+    ("one candidate too few", "const int V = n_select[b] < pn ? n_select[b] : pn;",
+     "const int V = n_select[b] <= pn ? n_select[b] - (n_select[b] > 1) : pn;", SELECT_PINS),
+    ("depth not incremented", "dep[i] = i == 0 ? 0 : dep[par[i]] + 1;",
+     "dep[i] = i == 0 ? 0 : dep[par[i]];", SELECT_PINS),
+    ("a child scoring above its parent accepted",
+     "if (i > 0 && sc[i] > sc[par[i]]) return LTDO_STATUS_BAD_SCORE;",
+     "if (i > 0 && sc[i] > sc[par[i]] + 1.0f) return LTDO_STATUS_BAD_SCORE;", SELECT_PINS),
 ]
 
 
@@ -103,7 +134,7 @@ def _pins_pass(pins):
 
 
 def test_unmutated_oracle_passes_every_pin():
-    assert _pins_pass(ATTN_PINS + ACCEPT_PINS + COMPACT_PINS)
+    assert _pins_pass(ATTN_PINS + ACCEPT_PINS + COMPACT_PINS + SELECT_PINS)
 
 
 @pytest.mark.parametrize("idx", range(len(MUTANTS)), ids=[m[0] for m in MUTANTS])

@@ -50,6 +50,26 @@ def test_eagle_pool_size_formula():
             W.tree_eagle(W.rng_for(2), pool + 1, D, W_, 1000)
 
 
+def test_draft_pool_levels_scores_and_selection_batches():
+    """The pool is listed level by level, its levels are true depths, scores
+    strictly decrease along every root path (also after float32 rounding they
+    never increase), and the selection batches pad with junk past each pool."""
+    for D in (1, 2, 6, 12):
+        p = W.draft_pool(W.rng_for(D), D, 10, 1000)
+        assert len(p.parents) == W.pool_size(D, 10)
+        assert _topological(p.parents)
+        assert (_levels(p.parents) == p.level).all() and (np.diff(p.level) >= 0).all()
+        assert (p.scores[1:] < p.scores[p.parents[1:]]).all()
+        s32 = p.scores.astype(np.float32)
+        assert (s32[1:] <= s32[p.parents[1:]]).all()
+    sb = W.select_batch16()
+    assert sb.Vpool == W.MAX_POOL and sb.pool_size.max() <= W.pool_size(12, 10) == 1011
+    assert set(sb.n_select.tolist()) <= {W.select_size_action(a) for a in range(12)}
+    for b in range(sb.B):
+        n = sb.pool_size[b]
+        assert (sb.pool_parents[b, n:] >= sb.Vpool).all() and (sb.pool_tokens[b, n:] < 0).all()
+
+
 @pytest.mark.parametrize("n,depth", [(8, 2), (8, 8), (64, 5), (256, 10)])
 def test_exact_depth_trees(n, depth):
     par = W.tree_random_exact_depth(W.rng_for(3), n, depth)
