@@ -13,6 +13,11 @@ reads cold data.  `eager_us` is the same K steps launched one by one from
 Python.  `roofline` describes the dominant call: algorithmic bytes per launch
 over its average duration (a graph of K such calls, timed the same way).
 `cpu_baseline` times the CPU oracle on the host on a bounded sample.
+
+The step before verification, candidate selection (the V most probable
+candidates of the draft pool flattened into the tree that is verified), is
+timed apart the same way on a pool of the workload's shape and reported under
+`kernels.select_candidates`; it is not part of `value`.
 """
 from __future__ import annotations
 
@@ -69,6 +74,13 @@ def make_workload(args):
         desc = ("70B-shaped bf16 batched paged tree verify: batch 16, 64 q / 8 kv heads, head_dim 128, "
                 "prefix U[1024,8192], 16-token blocks, tree N U[16,128], vocab 128256, greedy")
     return b, desc
+
+
+def select_workload(name):
+    """Candidate pools shaped like each verify workload's trees."""
+    from paper_2603_01639_amd import workloads as W
+    return {"c2": W.select_8b, "c3": W.select_8b, "c4": W.select_deep,
+            "c5": W.select_batch16}[name](0)
 
 
 def algorithmic_bytes(b):
@@ -217,6 +229,26 @@ def main():
     kernels["tree_verify_attn"]["TFLOP/s"] = round(
         flops / (per_call_us["tree_verify_attn"] * 1e-6) / 1e12, 2)
     kernels["kv_compact"] = {"us": round(per_call_us["kv_compact"], 3)}
+
+    # ---- candidate selection, outside the step (a graph of K calls)
+    sb = select_workload(args.workload)
+    sel_in = [to_dev(a) for a in (sb.scores, sb.pool_parents, sb.pool_tokens, sb.pool_size,
+                                  sb.n_select)]
+    sel_out = [torch.empty((sb.B, sb.Nmax), **i32) for _ in range(4)]
+    sel_n = torch.empty((sb.B,), **i32)
+
+    def select(i):
+        ltd.select_candidates(*sel_in, sel_out[1], sel_out[2], sel_n, selected=sel_out[0],
+                              depth=sel_out[3], stream=stream)
+
+    torch.cuda.synchronize()
+    g = graph_of(select, args.steps)
+    sel_us = 1e3 * timed(lambda i: g.replay(), 1) / args.steps
+    del g
+    kernels["select_candidates"] = {
+        "us": round(sel_us, 3), "workload": sb.label, "batch": sb.B,
+        "pool": sb.pool_size.tolist()[:16], "V": sb.n_select.tolist()[:16],
+        "in_value": False}
     dom = max(("tree_verify_attn", "tree_accept"), key=lambda n: per_call_us[n])
     traffic = read_traffic(args.traffic, args.workload, dom)
     roof = {"kernel": dom, "bound": "hbm", "achieved": kernels[dom]["GB/s"], "peak": HBM_PEAK_GBS,
@@ -251,19 +283,29 @@ def main():
     print(json.dumps(rec), flush=True)
 
 
-def read_traffic(path, workload, call):
-    """HBM bytes per launch of `call` from the counter summary: a line
-    `traffic <workload> <call> <bytes> <source hash>` whose hash still matches
-    the attention/accept sources (otherwise the kernel changed: null)."""
-    if not os.path.exists(path):
-        return None
+# The kernel sources behind each call's counters (launch plan included).
+CALL_SOURCES = {
+    "tree_verify_attn": ("attn_mfma.hip", "attn_plan.hip", "attn_rowwise.hip", "ltd_device.hpp"),
+    "tree_accept": ("accept.hip", "ltd_device.hpp"),
+}
+
+
+def source_digest(call):
     import hashlib
     src = os.path.join(ROOT, "paper_2603_01639_amd", "csrc")
     h = hashlib.sha256()
-    for f in sorted(os.listdir(src)):
-        if f.endswith((".hip", ".hpp")):
-            h.update(open(os.path.join(src, f), "rb").read())
-    digest = h.hexdigest()[:16]
+    for f in CALL_SOURCES[call]:
+        h.update(open(os.path.join(src, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(path, workload, call):
+    """HBM bytes per launch of `call` from the counter summary: a line
+    `traffic <workload> <call> <bytes> <source hash>` whose hash still matches
+    the call's kernel sources (otherwise the kernel changed: null)."""
+    if not os.path.exists(path):
+        return None
+    digest = source_digest(call)
     for line in open(path):
         parts = line.split()
         if len(parts) == 5 and parts[0] == "traffic" and parts[1] == workload and parts[2] == call:

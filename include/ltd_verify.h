@@ -21,6 +21,12 @@
  *                         paragraph: the remainder after the first error is
  *                         dropped).
  *
+ * The step before it has a call of its own:
+ *
+ *   ltd_select_candidates the V most probable candidates of the draft tree's
+ *                         pool, flattened into the tree the three calls above
+ *                         verify (section 3.2, "Candidate Token Selection").
+ *
  * Conventions for every call
  * --------------------------
  * - All array pointers are DEVICE pointers, owned by the caller.  The library
@@ -67,8 +73,10 @@ extern "C" {
 #define LTD_STATUS_BAD_PREFIX 3 /* prefix_len[b] < 0, > max_prefix, or rows past capacity */
 #define LTD_STATUS_BAD_BLOCK 4  /* a block id the sequence uses is outside [0, num_blocks) */
 #define LTD_STATUS_BAD_PATH 5   /* accepted path not 0 = p_0 < p_1 < ..., or n_accepted out of range */
+#define LTD_STATUS_BAD_SCORE 6  /* a pool score is NaN or above its parent's */
 
 #define LTD_MAX_NODES 256 /* largest Nmax (the paper's size policy spans V in [20, 240]) */
+#define LTD_MAX_POOL 1024 /* largest draft pool (1 + W + (D-2) W^2 = 1011 at W = 10, D = 12) */
 
 /*
  * Tree attention (section 3.2: candidates flattened with a tree attention
@@ -171,6 +179,45 @@ int ltd_kv_compact(void* k_cache, void* v_cache, const int32_t* block_table,
  * n_nodes > Nmax). */
 int ltd_tree_verify_attn_num_splits(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
                                     int dtype, int prefix, int n_nodes);
+
+/*
+ * Candidate token selection (section 3.2, "Candidate Token Selection"): of a
+ * draft tree's candidate pool, keep the V = min(n_select[b], pool_size[b])
+ * candidates with the highest cumulative path score and flatten them into a
+ * tree in the form the verification calls take.
+ *
+ * Ranking: score descending; equal scores (-0.0 equals +0.0) rank the
+ * shallower candidate first, then the lower pool index.  Since a child never
+ * scores above its parent, the kept candidates form a rooted subtree.  The
+ * flattened order is depth ascending, then score descending, then pool index
+ * ascending, so every parent precedes its children.
+ *
+ *   scores        [B][Vpool] float32: cumulative log-probability of each
+ *                 candidate (any order-preserving image of its path
+ *                 probability); never above its parent's, never NaN.
+ *   pool_parents  [B][Vpool] int32: pool_parents[b][0] = -1 (the root) and
+ *                 0 <= pool_parents[b][i] < i.
+ *   pool_tokens   [B][Vpool] int32: the candidate tokens (copied, not read).
+ *   pool_size     [B] int32 in [1, Vpool]; columns past it are never read.
+ *   n_select      [B] int32 in [1, Nmax]: the verification size asked for
+ *                 (the size policy's action).
+ *   Vpool         1 <= Vpool <= LTD_MAX_POOL; 1 <= Nmax <= LTD_MAX_NODES.
+ *   Outputs [B][Nmax] int32, rows k < V written, the rest untouched:
+ *   selected      pool index of flattened node k (may be NULL);
+ *   parents       parent of node k in the flattened order (-1 for the root);
+ *                 the tree the verification calls take;
+ *   tokens        token of node k (the verification's draft tokens);
+ *   depth         depth of node k (the root is 0; may be NULL);
+ *   n_nodes       [B] int32: V.
+ * With validate != 0, malformed data is reported as LTD_STATUS_BAD_NNODES
+ * (pool_size or n_select out of range), LTD_STATUS_BAD_PARENT or
+ * LTD_STATUS_BAD_SCORE, and then nothing is written.  No workspace.
+ */
+int ltd_select_candidates(const float* scores, const int32_t* pool_parents,
+                          const int32_t* pool_tokens, const int32_t* pool_size,
+                          const int32_t* n_select, int B, int Vpool, int Nmax, int32_t* selected,
+                          int32_t* parents, int32_t* tokens, int32_t* depth, int32_t* n_nodes,
+                          int validate, int32_t* status, void* stream);
 
 /* Library version string. */
 const char* ltd_version(void);

@@ -32,8 +32,10 @@ STATUS_BAD_PARENT = 2
 STATUS_BAD_PREFIX = 3
 STATUS_BAD_BLOCK = 4
 STATUS_BAD_PATH = 5
+STATUS_BAD_SCORE = 6
 
 MAX_NODES = 256
+MAX_POOL = 1024
 
 EXPORTED = (
     "ltd_tree_verify_attn_workspace_size",
@@ -43,6 +45,7 @@ EXPORTED = (
     "ltd_kv_compact",
     "ltd_tree_verify_attn_num_splits",
     "ltd_version",
+    "ltd_select_candidates",
 )
 
 
@@ -77,6 +80,8 @@ def lib() -> ctypes.CDLL:
         L.ltd_kv_compact.restype = i32
         L.ltd_tree_verify_attn_num_splits.argtypes = [i32] * 9
         L.ltd_tree_verify_attn_num_splits.restype = i32
+        L.ltd_select_candidates.argtypes = [P] * 5 + [i32] * 3 + [P] * 5 + [i32, P, P]
+        L.ltd_select_candidates.restype = i32
         L.ltd_version.argtypes = []
         L.ltd_version.restype = ctypes.c_char_p
         _lib = L
@@ -187,3 +192,17 @@ def kv_compact(k_cache, v_cache, prefix_len, new_prefix_len, accepted_nodes, n_a
         int(num_layers), int(layer_stride_elems), _dtype_code(k_cache), int(validate), _p(status),
         _stream(stream))
     _check("ltd_kv_compact", rc)
+
+
+def select_candidates(scores, pool_parents, pool_tokens, pool_size, n_select, parents, tokens,
+                      n_nodes, *, selected=None, depth=None, validate: bool = False, status=None,
+                      stream=None):
+    """Candidate token selection; see ``ltd_select_candidates``.  Pools are
+    ``[B][Vpool]``, outputs ``[B][Nmax]`` int32 CUDA (HIP) tensors."""
+    B, Vpool = scores.shape
+    Nmax = parents.shape[1]
+    rc = lib().ltd_select_candidates(
+        _p(scores), _p(pool_parents), _p(pool_tokens), _p(pool_size), _p(n_select), B, Vpool, Nmax,
+        _p(selected), _p(parents), _p(tokens), _p(depth), _p(n_nodes), int(validate), _p(status),
+        _stream(stream))
+    _check("ltd_select_candidates", rc)

@@ -162,4 +162,29 @@ int ltd_kv_compact(void* k_cache, void* v_cache, const int32_t* block_table,
   return LTD_OK;
 }
 
+int ltd_select_candidates(const float* scores, const int32_t* pool_parents,
+                          const int32_t* pool_tokens, const int32_t* pool_size,
+                          const int32_t* n_select, int B, int Vpool, int Nmax, int32_t* selected,
+                          int32_t* parents, int32_t* tokens, int32_t* depth, int32_t* n_nodes,
+                          int validate, int32_t* status, void* stream) {
+  if (B < 0 || Vpool < 1 || Vpool > LTD_MAX_POOL || Nmax < 1 || Nmax > LTD_MAX_NODES)
+    return LTD_EINVAL;
+  if (validate && !status) return LTD_EINVAL;
+  if (B == 0) return LTD_OK;
+  if (!scores || !pool_parents || !pool_tokens || !pool_size || !n_select || !parents ||
+      !tokens || !n_nodes)
+    return LTD_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (validate) {
+    if (ltd::launch_validate_pool(scores, pool_parents, pool_size, n_select, B, Vpool, Nmax,
+                                  status, st) != hipSuccess)
+      return LTD_EHIP;
+  }
+  if (ltd::launch_select(scores, pool_parents, pool_tokens, pool_size, n_select, B, Vpool, Nmax,
+                         selected, parents, tokens, depth, n_nodes, validate ? status : nullptr,
+                         st) != hipSuccess)
+    return LTD_EHIP;
+  return LTD_OK;
+}
+
 }  // extern "C"

@@ -55,4 +55,15 @@ hipError_t launch_compact(void* k_cache, void* v_cache, const int32_t* block_tab
                           int num_layers, int64_t layer_stride_bytes, const int32_t* status,
                           hipStream_t stream);
 
+// select.hip
+int select_block_threads(int Vpool);
+hipError_t launch_validate_pool(const float* scores, const int32_t* pool_parents,
+                                const int32_t* pool_size, const int32_t* n_select, int B,
+                                int Vpool, int Nmax, int32_t* status, hipStream_t stream);
+hipError_t launch_select(const float* scores, const int32_t* pool_parents,
+                         const int32_t* pool_tokens, const int32_t* pool_size,
+                         const int32_t* n_select, int B, int Vpool, int Nmax, int32_t* selected,
+                         int32_t* parents, int32_t* tokens, int32_t* depth, int32_t* n_nodes,
+                         const int32_t* status, hipStream_t stream);
+
 }  // namespace ltd

@@ -17,9 +17,10 @@ def _declared():
     return sorted(set(re.findall(r"\b(ltd_[a-z_0-9]+)\s*\(", text)))
 
 
-def test_header_declares_the_three_steps():
+def test_header_declares_the_three_steps_and_the_selection():
     names = _declared()
-    for fn in ("ltd_tree_verify_attn", "ltd_tree_accept", "ltd_kv_compact"):
+    for fn in ("ltd_tree_verify_attn", "ltd_tree_accept", "ltd_kv_compact",
+               "ltd_select_candidates"):
         assert fn in names
 
 
@@ -97,3 +98,23 @@ def test_attention_rejects_a_scale_that_is_not_positive_and_finite(scale):
     rc = ltd.lib().ltd_tree_verify_attn(P, P, P, None, P, P, P, P, 1, 4, 8, 2, 128, 64, 128, 0, 0,
                                         scale, ltd.DTYPE_BF16, None, 0, 0, None, None)
     assert rc == ltd.LTD_EINVAL
+
+
+@pytest.mark.parametrize("B,Vpool,Nmax,validate,status", [
+    (-1, 411, 60, 0, None), (1, 0, 60, 0, None), (1, ltd.MAX_POOL + 1, 60, 0, None),
+    (1, 411, 0, 0, None), (1, 411, ltd.MAX_NODES + 1, 0, None), (1, 411, 60, 1, None)])
+def test_selection_rejects_bad_scalar_arguments(B, Vpool, Nmax, validate, status):
+    """Pool width, output rows, batch size and a missing status buffer are
+    checked on the host before anything is launched (dummy pointers)."""
+    P = 0x1000
+    rc = ltd.lib().ltd_select_candidates(P, P, P, P, P, B, Vpool, Nmax, P, P, P, P, P, validate,
+                                         status, None)
+    assert rc == ltd.LTD_EINVAL
+
+
+def test_selection_of_an_empty_batch_launches_nothing():
+    assert ltd.lib().ltd_select_candidates(None, None, None, None, None, 0, 1024, 256, None, None,
+                                           None, None, None, 0, None, None) == ltd.LTD_OK
+    P = 0x1000  # a required output missing
+    assert ltd.lib().ltd_select_candidates(P, P, P, P, P, 1, 16, 16, P, None, P, P, P, 0, None,
+                                           None) == ltd.LTD_EINVAL
