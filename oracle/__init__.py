@@ -175,9 +175,9 @@ def kv_compact(k_cache, v_cache, prefix_len, accepted_nodes, n_accepted, *, Hkv,
 
 def select_candidates(scores, pool_parents, pool_tokens, pool_size, n_select, Nmax):
     """Candidate token selection (section 3.2): the V = min(n_select, pool
-    size) candidates of highest cumulative score, flattened in (depth, score,
-    pool index) order.  Returns (selected, parents, tokens, depth, n_nodes);
-    entries past V hold -1."""
+    size) candidates of highest cumulative score (equal scores: lower pool
+    index first), flattened in pool order.  Returns (selected, parents,
+    tokens, depth, n_nodes); entries past V hold -1."""
     scores = np.ascontiguousarray(scores, np.float32)
     B, Vpool = scores.shape
     pool_parents = np.ascontiguousarray(pool_parents, np.int32)

@@ -341,13 +341,13 @@ int ltd_oracle_kv_compact(void* k_cache, void* v_cache, const int32_t* block_tab
 /* ---- candidate token selection (section 3.2, "Candidate Token Selection").
  * The paper keeps the V candidates of the draft tree with the highest overall
  * (cumulative path) probability.  Readings of what it leaves open: equal
- * scores are ranked by depth, then pool index (a parent never ranks below its
- * child, since its score is not lower and its depth is), which keeps the kept
- * set a rooted subtree; the flattened order is by depth, then score, then
- * pool index, which puts every parent before its children. */
+ * scores are ranked by pool index, lower first (the pool lists a parent before
+ * its children and a child never scores above its parent, so a parent always
+ * ranks before its children and the kept set is a rooted subtree); the kept
+ * candidates are flattened in pool order, which puts every parent before its
+ * children (and, for a pool listed level by level, is depth-major). */
 typedef struct {
   float score;
-  int depth;
   int index;
 } cand_t;
 
@@ -355,15 +355,12 @@ static int by_rank(const void* pa, const void* pb) {
   const cand_t* a = (const cand_t*)pa;
   const cand_t* b = (const cand_t*)pb;
   if (a->score != b->score) return a->score > b->score ? -1 : 1;
-  if (a->depth != b->depth) return a->depth < b->depth ? -1 : 1;
   return (a->index > b->index) - (a->index < b->index);
 }
 
-static int by_flat_order(const void* pa, const void* pb) {
+static int by_pool_order(const void* pa, const void* pb) {
   const cand_t* a = (const cand_t*)pa;
   const cand_t* b = (const cand_t*)pb;
-  if (a->depth != b->depth) return a->depth < b->depth ? -1 : 1;
-  if (a->score != b->score) return a->score > b->score ? -1 : 1;
   return (a->index > b->index) - (a->index < b->index);
 }
 
@@ -406,14 +403,13 @@ int ltd_oracle_select_candidates(const float* scores, const int32_t* pool_parent
     for (int i = 0; i < pn; ++i) dep[i] = i == 0 ? 0 : dep[par[i]] + 1;
     for (int i = 0; i < pn; ++i) {
       c[i].score = sc[i];
-      c[i].depth = dep[i];
       c[i].index = i;
     }
     /* the V candidates ranked first */
     qsort(c, (size_t)pn, sizeof(cand_t), by_rank);
     const int V = n_select[b] < pn ? n_select[b] : pn;
-    /* flattened: depth, then score, then pool index */
-    qsort(c, (size_t)V, sizeof(cand_t), by_flat_order);
+    /* flattened in pool order */
+    qsort(c, (size_t)V, sizeof(cand_t), by_pool_order);
     for (int i = 0; i < pn; ++i) new_id[i] = -1;
     for (int k = 0; k < V; ++k) new_id[c[k].index] = k;
     const int64_t o = (int64_t)b * Nmax;
@@ -422,7 +418,7 @@ int ltd_oracle_select_candidates(const float* scores, const int32_t* pool_parent
       selected[o + k] = j;
       parents[o + k] = j == 0 ? -1 : new_id[par[j]];
       tokens[o + k] = pool_tokens[(int64_t)b * Vpool + j];
-      depth[o + k] = c[k].depth;
+      depth[o + k] = dep[j];
     }
     n_nodes[b] = V;
   }

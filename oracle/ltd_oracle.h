@@ -73,10 +73,9 @@ int ltd_oracle_kv_compact(void* k_cache, void* v_cache, const int32_t* block_tab
  * [B][Vpool], pool_parents[b][0] = -1 and 0 <= pool_parents[b][i] < i; a
  * cumulative score per candidate, larger = more probable, never above its
  * parent's), keep the V = min(n_select[b], pool_size[b]) candidates ranked
- * first by (score descending, depth ascending, pool index ascending), and
- * flatten them in (depth ascending, score descending, pool index ascending)
- * order.  Outputs [B][Nmax] (entries past V untouched): selected = pool
- * index of node k, parents in the new order (-1 for the root), tokens, depth;
+ * first by (score descending, pool index ascending), and flatten them in pool
+ * order.  Outputs [B][Nmax] (entries past V untouched): selected = pool index
+ * of node k, parents in the new order (-1 for the root), tokens, depth;
  * n_nodes[b] = V. */
 int ltd_oracle_select_candidates(const float* scores, const int32_t* pool_parents,
                                  const int32_t* pool_tokens, const int32_t* pool_size,

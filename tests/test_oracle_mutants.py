@@ -85,20 +85,24 @@ MUTANTS = [
      COMPACT_PINS),
     ("compaction shifts by one row", "int64_t off = cache_row_offset(block_table, b, g, P + j, Hkv",
      "int64_t off = cache_row_offset(block_table, b, g, P + j + 1, Hkv", COMPACT_PINS),
-    ("selection ties ignore depth",
-     "if (a->depth != b->depth) return a->depth < b->depth ? -1 : 1;\n  return (a->index > b->index)",
-     "return (a->index > b->index)", SELECT_PINS),
+    ("selection ties go to the higher index",
+     "if (a->score != b->score) return a->score > b->score ? -1 : 1;\n"
+     "  return (a->index > b->index) - (a->index < b->index);",
+     "if (a->score != b->score) return a->score > b->score ? -1 : 1;\n"
+     "  return (a->index < b->index) - (a->index > b->index);", SELECT_PINS),
     ("selection keeps the lowest scores",
-     "if (a->score != b->score) return a->score > b->score ? -1 : 1;\n  if (a->depth",
-     "if (a->score != b->score) return a->score < b->score ? -1 : 1;\n  if (a->depth", SELECT_PINS),
-    ("flattened order ignores depth",
-     "if (a->depth != b->depth) return a->depth < b->depth ? -1 : 1;\n  if (a->score",
-     "if (a->score", SELECT_PINS),
-    ("flattened order ignores score",
-     "  if (a->score != b->score) return a->score > b->score ? -1 : 1;\n"
-     "  return (a->index > b->index) - (a->index < b->index);\n}\n\nint ltd_oracle_select",
-     "  return (a->index > b->index) - (a->index < b->index);\n}\n\nint ltd_oracle_select",
+     "if (a->score != b->score) return a->score > b->score ? -1 : 1;\n  return (a->index",
+     "if (a->score != b->score) return a->score < b->score ? -1 : 1;\n  return (a->index",
      SELECT_PINS),
+    ("flattened in rank order", "qsort(c, (size_t)V, sizeof(cand_t), by_pool_order);",
+     "(void)by_pool_order;", SELECT_PINS),
+    ("flattened in reverse pool order",
+     "static int by_pool_order(const void* pa, const void* pb) {\n"
+     "  const cand_t* a = (const cand_t*)pa;\n  const cand_t* b = (const cand_t*)pb;\n"
+     "  return (a->index > b->index) - (a->index < b->index);",
+     "static int by_pool_order(const void* pa, const void* pb) {\n"
+     "  const cand_t* a = (const cand_t*)pa;\n  const cand_t* b = (const cand_t*)pb;\n"
+     "  return (a->index < b->index) - (a->index > b->index);", SELECT_PINS),
     ("parents left as pool indices", "parents[o + k] = j == 0 ? -1 : new_id[par[j]];",
      "parents[o + k] = j == 0 ? -1 : par[j];", SELECT_PINS),
     ("one candidate too few", "const int V = n_select[b] < pn ? n_select[b] : pn;",
