@@ -237,9 +237,9 @@ def main():
     sel_out = [torch.empty((sb.B, sb.Nmax), **i32) for _ in range(4)]
     sel_n = torch.empty((sb.B,), **i32)
 
-    def select(i):
+    def select(i):  # the outputs verification reads, plus the pool indices; no depths
         ltd.select_candidates(*sel_in, sel_out[1], sel_out[2], sel_n, selected=sel_out[0],
-                              depth=sel_out[3], stream=stream)
+                              stream=stream)
 
     torch.cuda.synchronize()
     g = graph_of(select, args.steps)
@@ -248,7 +248,7 @@ def main():
     kernels["select_candidates"] = {
         "us": round(sel_us, 3), "workload": sb.label, "batch": sb.B,
         "pool": sb.pool_size.tolist()[:16], "V": sb.n_select.tolist()[:16],
-        "in_value": False}
+        "outputs": "parents, tokens, n_nodes, selected", "in_value": False}
     dom = max(("tree_verify_attn", "tree_accept"), key=lambda n: per_call_us[n])
     traffic = read_traffic(args.traffic, args.workload, dom)
     roof = {"kernel": dom, "bound": "hbm", "achieved": kernels[dom]["GB/s"], "peak": HBM_PEAK_GBS,

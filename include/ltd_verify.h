@@ -186,11 +186,11 @@ int ltd_tree_verify_attn_num_splits(int B, int Nmax, int Hq, int Hkv, int d, int
  * candidates with the highest cumulative path score and flatten them into a
  * tree in the form the verification calls take.
  *
- * Ranking: score descending; equal scores (-0.0 equals +0.0) rank the
- * shallower candidate first, then the lower pool index.  Since a child never
- * scores above its parent, the kept candidates form a rooted subtree.  The
- * flattened order is depth ascending, then score descending, then pool index
- * ascending, so every parent precedes its children.
+ * Ranking: score descending; equal scores (-0.0 equals +0.0) rank the lower
+ * pool index first.  Since the pool lists a parent before its children and a
+ * child never scores above its parent, the kept candidates form a rooted
+ * subtree.  They are flattened in pool order, so every parent precedes its
+ * children (and a pool listed level by level comes out depth-major).
  *
  *   scores        [B][Vpool] float32: cumulative log-probability of each
  *                 candidate (any order-preserving image of its path
@@ -207,7 +207,8 @@ int ltd_tree_verify_attn_num_splits(int B, int Nmax, int Hq, int Hkv, int d, int
  *   parents       parent of node k in the flattened order (-1 for the root);
  *                 the tree the verification calls take;
  *   tokens        token of node k (the verification's draft tokens);
- *   depth         depth of node k (the root is 0; may be NULL);
+ *   depth         depth of node k (the root is 0; may be NULL, which saves
+ *                 the pass that computes it);
  *   n_nodes       [B] int32: V.
  * With validate != 0, malformed data is reported as LTD_STATUS_BAD_NNODES
  * (pool_size or n_select out of range), LTD_STATUS_BAD_PARENT or
