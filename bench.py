@@ -14,10 +14,12 @@ Python.  `roofline` describes the dominant call: algorithmic bytes per launch
 over its average duration (a graph of K such calls, timed the same way).
 `cpu_baseline` times the CPU oracle on the host on a bounded sample.
 
-The step before verification, candidate selection (the V most probable
-candidates of the draft pool flattened into the tree that is verified), is
-timed apart the same way on a pool of the workload's shape and reported under
-`kernels.select_candidates`; it is not part of `value`.
+The steps before verification are timed apart the same way and reported
+under `kernels`, not in `value`: candidate selection (the V most probable
+candidates of the draft pool flattened into the tree that is verified) on a
+pool of the workload's shape (`select_candidates`), and the size and depth
+policies' inference on one state per sequence (`size_policy`,
+`depth_policy`; random weights of the paper's shapes).
 """
 from __future__ import annotations
 
@@ -249,6 +251,34 @@ def main():
         "us": round(sel_us, 3), "workload": sb.label, "batch": sb.B,
         "pool": sb.pool_size.tolist()[:16], "V": sb.n_select.tolist()[:16],
         "outputs": "parents, tokens, n_nodes, selected", "in_value": False}
+
+    # ---- draft policies, outside the step (graphs of K calls), one state
+    # per sequence of the workload
+    from paper_2603_01639_amd import workloads as W
+    for layout, name in ((W.LAYOUT_SIZE, "size_policy"), (W.LAYOUT_DEPTH, "depth_policy")):
+        pb = W.policy_batch(layout, b.B)
+        layers = [(to_dev(w), to_dev(bias)) for w, bias in pb.layers]
+        p_in = [to_dev(a) for a in (pb.scores, pb.pool_size, pb.depth, pb.ctx_len)]
+        p_logits = torch.empty((pb.B, pb.dims[-1]), dtype=torch.float32, device="cuda")
+        p_action = torch.empty((pb.B,), **i32)
+        p_ws = torch.empty(ltd.policy_workspace_size(pb.B, pb.dims[1],
+                                                     pb.dims[2] if len(pb.dims) == 4 else 0),
+                           dtype=torch.uint8, device="cuda")
+
+        def policy(i, layout=layout, layers=layers, p_in=p_in, p_logits=p_logits,
+                   p_action=p_action, p_ws=p_ws, pb=pb):
+            ltd.policy_forward(layout, *p_in, layers, p_logits, p_action, pad=W.STATE_PAD,
+                               action_offset=pb.action_offset, action_scale=pb.action_scale,
+                               workspace=p_ws, stream=stream)
+
+        torch.cuda.synchronize()
+        g = graph_of(policy, args.steps)
+        p_us = 1e3 * timed(lambda i: g.replay(), 1) / args.steps
+        del g
+        wbytes = int(sum(w.nbytes + bias.nbytes for w, bias in pb.layers))
+        kernels[name] = {"us": round(p_us, 3), "batch": pb.B, "dims": list(pb.dims),
+                         "weight_bytes": wbytes,
+                         "GB/s": round(wbytes / (p_us * 1e-6) / 1e9, 1), "in_value": False}
     dom = max(("tree_verify_attn", "tree_accept"), key=lambda n: per_call_us[n])
     traffic = read_traffic(args.traffic, args.workload, dom)
     roof = {"kernel": dom, "bound": "hbm", "achieved": kernels[dom]["GB/s"], "peak": HBM_PEAK_GBS,

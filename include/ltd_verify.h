@@ -78,6 +78,12 @@ extern "C" {
 #define LTD_MAX_NODES 256 /* largest Nmax (the paper's size policy spans V in [20, 240]) */
 #define LTD_MAX_POOL 1024 /* largest draft pool (1 + W + (D-2) W^2 = 1011 at W = 10, D = 12) */
 
+#define LTD_POLICY_SIZE 0          /* state [D, L, score of every pool candidate, pad ...] */
+#define LTD_POLICY_DEPTH 1         /* state [scores of the newest in_dim-2 candidates, D, L] */
+#define LTD_POLICY_MAX_IN 1024     /* state width (the size policy's is 2 + 1011) */
+#define LTD_POLICY_MAX_HIDDEN 1024 /* hidden width (the paper's widest layer) */
+#define LTD_POLICY_MAX_OUT 64      /* output logits (12 size actions, 2 depth actions) */
+
 /*
  * Tree attention (section 3.2: candidates flattened with a tree attention
  * mask, verified in one target pass).
@@ -219,6 +225,41 @@ int ltd_select_candidates(const float* scores, const int32_t* pool_parents,
                           const int32_t* n_select, int B, int Vpool, int Nmax, int32_t* selected,
                           int32_t* parents, int32_t* tokens, int32_t* depth, int32_t* n_nodes,
                           int validate, int32_t* status, void* stream);
+
+/*
+ * Draft-policy inference (section 4: the state vector of draft depth D,
+ * context length L and candidate scores; appendix A.2: the size and depth
+ * policies are fully connected ReLU networks with hidden widths [1024, 256]
+ * and [1024], 12 and 2 actions, the action being the most likely one).
+ *
+ * The state of sequence b is built from its draft pool (no separate pass):
+ *   LTD_POLICY_SIZE   [D_b, L_b, scores[b][0 .. min(n_b, F)), pad ...]
+ *   LTD_POLICY_DEPTH  [pad ..., scores[b][n_b - F .. n_b), D_b, L_b]
+ * with n_b = pool_size[b] and F = in_dim - 2 (the depth layout takes the last
+ * F candidates, i.e. the newest expansion once the pool holds W^2 of them).
+ * Then h1 = relu(w1 s + b1), optionally h2 = relu(w2 h1 + b2) (h2 > 0), and
+ * logits = wo h + bo; action[b] = action_offset + action_scale * argmax
+ * (lowest index on ties), so the size policy's V = 20 + 20 a can be written
+ * straight into ltd_select_candidates' n_select.
+ *
+ *   scores [B][Vpool] float32, pool_size/depth/ctx_len [B] int32 (read).
+ *   w1 [h1][in_dim], b1 [h1]; w2 [h2][h1], b2 [h2] (NULL when h2 = 0);
+ *   wo [n_out][h2 or h1], bo [n_out]: float32, row-major (a row per unit).
+ *   logits [B][n_out] float32, action [B] int32 (written).
+ *   workspace: ltd_policy_workspace_size(B, h1, h2) bytes (hidden activations).
+ * Limits: 3 <= in_dim <= LTD_POLICY_MAX_IN, 1 <= h1 <= LTD_POLICY_MAX_HIDDEN,
+ * 0 <= h2 <= LTD_POLICY_MAX_HIDDEN, 1 <= n_out <= LTD_POLICY_MAX_OUT;
+ * anything else, or a bad layout, is LTD_EINVAL.  Accumulation is float32 in
+ * a fixed order (deterministic).
+ */
+size_t ltd_policy_workspace_size(int B, int h1, int h2);
+
+int ltd_policy_forward(int layout, const float* scores, const int32_t* pool_size, int Vpool,
+                       const int32_t* depth, const int32_t* ctx_len, float pad, int B, int in_dim,
+                       const float* w1, const float* b1, int h1, const float* w2, const float* b2,
+                       int h2, const float* wo, const float* bo, int n_out, int action_offset,
+                       int action_scale, float* logits, int32_t* action, void* workspace,
+                       size_t workspace_bytes, void* stream);
 
 /* Library version string. */
 const char* ltd_version(void);

@@ -36,6 +36,8 @@ STATUS_BAD_SCORE = 6
 
 MAX_NODES = 256
 MAX_POOL = 1024
+POLICY_SIZE = 0
+POLICY_DEPTH = 1
 
 EXPORTED = (
     "ltd_tree_verify_attn_workspace_size",
@@ -46,6 +48,8 @@ EXPORTED = (
     "ltd_tree_verify_attn_num_splits",
     "ltd_version",
     "ltd_select_candidates",
+    "ltd_policy_workspace_size",
+    "ltd_policy_forward",
 )
 
 
@@ -82,6 +86,11 @@ def lib() -> ctypes.CDLL:
         L.ltd_tree_verify_attn_num_splits.restype = i32
         L.ltd_select_candidates.argtypes = [P] * 5 + [i32] * 3 + [P] * 5 + [i32, P, P]
         L.ltd_select_candidates.restype = i32
+        L.ltd_policy_workspace_size.argtypes = [i32] * 3
+        L.ltd_policy_workspace_size.restype = sz
+        L.ltd_policy_forward.argtypes = ([i32, P, P, i32, P, P, f32, i32, i32, P, P, i32, P, P, i32,
+                                          P, P, i32, i32, i32, P, P, P, sz, P])
+        L.ltd_policy_forward.restype = i32
         L.ltd_version.argtypes = []
         L.ltd_version.restype = ctypes.c_char_p
         _lib = L
@@ -206,3 +215,30 @@ def select_candidates(scores, pool_parents, pool_tokens, pool_size, n_select, pa
         _p(selected), _p(parents), _p(tokens), _p(depth), _p(n_nodes), int(validate), _p(status),
         _stream(stream))
     _check("ltd_select_candidates", rc)
+
+
+def policy_workspace_size(B, h1, h2) -> int:
+    return int(lib().ltd_policy_workspace_size(B, h1, h2))
+
+
+def policy_forward(layout, scores, pool_size, depth, ctx_len, layers, logits, action, *,
+                   pad: float = -100.0, action_offset: int = 0, action_scale: int = 1,
+                   workspace=None, stream=None):
+    """Draft-policy inference; see ``ltd_policy_forward``.  ``layers`` is a
+    list of (W [out][in], b [out]) float32 CUDA tensors: two or three layers
+    (one or two hidden ReLU layers, then the output layer)."""
+    if len(layers) not in (2, 3):
+        raise ValueError("a policy has one or two hidden layers")
+    B, Vpool = scores.shape
+    (w1, b1), *mid, (wo, bo) = layers
+    w2, b2 = mid[0] if mid else (None, None)
+    h1 = w1.shape[0]
+    h2 = 0 if w2 is None else w2.shape[0]
+    if workspace is None:
+        workspace = _alloc_workspace(policy_workspace_size(B, h1, h2), scores.device)
+    rc = lib().ltd_policy_forward(
+        int(layout), _p(scores), _p(pool_size), Vpool, _p(depth), _p(ctx_len), float(pad), B,
+        w1.shape[1], _p(w1), _p(b1), h1, _p(w2), _p(b2), h2, _p(wo), _p(bo), wo.shape[0],
+        int(action_offset), int(action_scale), _p(logits), _p(action), _p(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream))
+    _check("ltd_policy_forward", rc)

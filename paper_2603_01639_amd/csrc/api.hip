@@ -187,4 +187,33 @@ int ltd_select_candidates(const float* scores, const int32_t* pool_parents,
   return LTD_OK;
 }
 
+size_t ltd_policy_workspace_size(int B, int h1, int h2) {
+  if (B < 0 || h1 < 1 || h1 > LTD_POLICY_MAX_HIDDEN || h2 < 0 || h2 > LTD_POLICY_MAX_HIDDEN)
+    return 0;
+  return ltd::policy_workspace_bytes(B, h1, h2);
+}
+
+int ltd_policy_forward(int layout, const float* scores, const int32_t* pool_size, int Vpool,
+                       const int32_t* depth, const int32_t* ctx_len, float pad, int B, int in_dim,
+                       const float* w1, const float* b1, int h1, const float* w2, const float* b2,
+                       int h2, const float* wo, const float* bo, int n_out, int action_offset,
+                       int action_scale, float* logits, int32_t* action, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  if ((layout != LTD_POLICY_SIZE && layout != LTD_POLICY_DEPTH) || B < 0 || Vpool < 1 ||
+      in_dim < 3 || in_dim > LTD_POLICY_MAX_IN || h1 < 1 || h1 > LTD_POLICY_MAX_HIDDEN || h2 < 0 ||
+      h2 > LTD_POLICY_MAX_HIDDEN || n_out < 1 || n_out > LTD_POLICY_MAX_OUT)
+    return LTD_EINVAL;
+  if (B == 0) return LTD_OK;
+  if (!scores || !pool_size || !depth || !ctx_len || !w1 || !b1 || !wo || !bo || !logits ||
+      !action || (h2 > 0 && (!w2 || !b2)))
+    return LTD_EINVAL;
+  if (!workspace || workspace_bytes < ltd::policy_workspace_bytes(B, h1, h2))
+    return LTD_EWORKSPACE;
+  if (ltd::launch_policy(layout, scores, pool_size, Vpool, depth, ctx_len, pad, B, in_dim, w1, b1,
+                         h1, w2, b2, h2, wo, bo, n_out, action_offset, action_scale, logits, action,
+                         workspace, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return LTD_EHIP;
+  return LTD_OK;
+}
+
 }  // extern "C"

@@ -66,4 +66,13 @@ hipError_t launch_select(const float* scores, const int32_t* pool_parents,
                          int32_t* parents, int32_t* tokens, int32_t* depth, int32_t* n_nodes,
                          const int32_t* status, hipStream_t stream);
 
+// policy.hip
+size_t policy_workspace_bytes(int B, int h1, int h2);
+hipError_t launch_policy(int layout, const float* scores, const int32_t* pool_size, int Vpool,
+                         const int32_t* depth, const int32_t* ctx_len, float pad, int B,
+                         int in_dim, const float* w1, const float* b1, int h1, const float* w2,
+                         const float* b2, int h2, const float* wo, const float* bo, int n_out,
+                         int action_offset, int action_scale, float* logits, int32_t* action,
+                         void* workspace, hipStream_t stream);
+
 }  // namespace ltd

@@ -462,3 +462,64 @@ def select_batch16(rep: int = 0) -> SelectBatch:
     pools = [draft_pool(rng, D, 10, 128256) for D in depths]
     return make_select_batch(pools, vs, Vpool=MAX_POOL, Nmax=256,
                              label="select B16 D1-12 W10 V20-240")
+
+
+# ------------------------------------------------------------ draft policies
+
+LAYOUT_SIZE = 0  # state [D, L, scores of every pool candidate, pad]
+LAYOUT_DEPTH = 1  # state [scores of the newest W^2 candidates, D, L]
+SIZE_POLICY_DIMS = (2 + 1011, 1024, 256, 12)  # appendix A.2: hidden [1024, 256], 12 actions
+DEPTH_POLICY_DIMS = (2 + 100, 1024, 2)  # hidden [1024], CONTINUE / STOP
+STATE_PAD = -100.0  # the score written past a pool's end
+
+
+def policy_layers(rng: np.random.Generator, dims) -> List[tuple]:
+    """Random weights of a ReLU network (trained weights are not available):
+    per layer W [out][in] and b [out], uniform in +-1/sqrt(in) (the usual
+    default initialisation of a fully connected layer), float32."""
+    out = []
+    for i, o in zip(dims[:-1], dims[1:]):
+        k = 1.0 / np.sqrt(i)
+        out.append((rng.uniform(-k, k, size=(o, i)).astype(np.float32),
+                    rng.uniform(-k, k, size=o).astype(np.float32)))
+    return out
+
+
+@dataclasses.dataclass
+class PolicyBatch:
+    """Pool scores of B sequences plus their draft depth and context length,
+    and a random-weight network of the paper's shape."""
+    layout: int
+    dims: tuple
+    layers: List[tuple]
+    scores: np.ndarray  # float32 [B][Vpool]
+    pool_size: np.ndarray  # int32 [B]
+    depth: np.ndarray  # int32 [B]
+    ctx_len: np.ndarray  # int32 [B]
+    action_offset: int
+    action_scale: int
+    label: str = ""
+    pool_parents: Optional[np.ndarray] = None  # int32 [B][Vpool] (the pools behind the scores)
+    pool_tokens: Optional[np.ndarray] = None  # int32 [B][Vpool]
+
+    @property
+    def B(self) -> int:
+        return self.scores.shape[0]
+
+
+def policy_batch(layout: int, B: int, rep: int = 0) -> PolicyBatch:
+    """B sequences, each with a depth-D, width-10 draft pool (D uniform in
+    [2, 12]) and a context length uniform in [128, 16384]; the size policy's
+    actions map to V = 20 + 20 a."""
+    rng = rng_for(config_seed(9 + layout, rep) * 100 + B)
+    dims = SIZE_POLICY_DIMS if layout == LAYOUT_SIZE else DEPTH_POLICY_DIMS
+    layers = policy_layers(rng, dims)
+    depths = [int(rng.integers(2, 13)) for _ in range(B)]
+    pools = [draft_pool(rng, D, 10, 128256) for D in depths]
+    sb = make_select_batch(pools, [1] * B, Vpool=MAX_POOL)
+    ctx = rng.integers(128, 16385, size=B).astype(np.int32)
+    off, scale = (20, 20) if layout == LAYOUT_SIZE else (0, 1)
+    name = "size" if layout == LAYOUT_SIZE else "depth"
+    return PolicyBatch(layout, dims, layers, sb.scores, sb.pool_size, np.array(depths, np.int32),
+                       ctx, off, scale, label=f"{name} policy B{B} dims {dims}",
+                       pool_parents=sb.pool_parents, pool_tokens=sb.pool_tokens)

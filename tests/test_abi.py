@@ -118,3 +118,27 @@ def test_selection_of_an_empty_batch_launches_nothing():
     P = 0x1000  # a required output missing
     assert ltd.lib().ltd_select_candidates(P, P, P, P, P, 1, 16, 16, P, None, P, P, P, 0, None,
                                            None) == ltd.LTD_EINVAL
+
+
+@pytest.mark.parametrize("args", [
+    dict(layout=2), dict(B=-1), dict(Vpool=0), dict(in_dim=2), dict(in_dim=1025), dict(h1=0),
+    dict(h1=1025), dict(h2=-1), dict(h2=1025), dict(n_out=0), dict(n_out=65)])
+def test_policy_rejects_bad_scalar_arguments(args):
+    P = 0x1000
+    a = dict(layout=0, B=2, Vpool=1024, in_dim=1013, h1=1024, h2=256, n_out=12)
+    a.update(args)
+    rc = ltd.lib().ltd_policy_forward(a["layout"], P, P, a["Vpool"], P, P, -100.0, a["B"],
+                                      a["in_dim"], P, P, a["h1"], P, P, a["h2"], P, P, a["n_out"],
+                                      20, 20, P, P, P, 1 << 30, None)
+    assert rc == ltd.LTD_EINVAL
+
+
+def test_policy_workspace_and_missing_buffers():
+    assert ltd.policy_workspace_size(16, 1024, 256) == 16 * (1024 + 256) * 4
+    assert ltd.policy_workspace_size(1, 1024, 0) == 1024 * 4
+    P = 0x1000
+    # h2 > 0 needs w2/b2; too small a workspace is LTD_EWORKSPACE
+    assert ltd.lib().ltd_policy_forward(0, P, P, 16, P, P, 0.0, 1, 10, P, P, 8, None, None, 4, P,
+                                        P, 2, 0, 1, P, P, P, 1 << 20, None) == ltd.LTD_EINVAL
+    assert ltd.lib().ltd_policy_forward(0, P, P, 16, P, P, 0.0, 1, 10, P, P, 8, P, P, 4, P, P, 2,
+                                        0, 1, P, P, P, 4, None) == ltd.LTD_EWORKSPACE

@@ -148,3 +148,55 @@ def test_every_mutant_is_caught(idx, tmp_path, monkeypatch):
     monkeypatch.setattr(oracle, "_lib", oracle.load_library(so))
     np.seterr(all="ignore")
     assert not _pins_pass(pins), f"pins did not notice: {name}"
+
+
+# ---- the policy oracle (numpy): the same idea, planted in a copy of its source
+import importlib.util  # noqa: E402
+
+import test_oracle_policy as TP  # noqa: E402
+from oracle import policy as _policy  # noqa: E402
+
+POLICY_PINS = [
+    lambda: TP.test_worked_examples(),
+    lambda: TP.test_matches_torch_linear_relu_stack((7, 5, 3)),
+    lambda: TP.test_zero_weights_give_the_bias_and_the_action_map(),
+    lambda: TP.test_state_layouts(),
+]
+POLICY_MUTANTS = [
+    ("ReLU missing", "h = np.maximum(h, 0.0)", "h = h"),
+    ("bias dropped", "h = h @ np.asarray(w, np.float64).T + np.asarray(bias, np.float64)",
+     "h = h @ np.asarray(w, np.float64).T"),
+    ("ReLU on the logits too", "if k + 1 < len(layers):", "if True:"),
+    ("argmax ties to the last index", "np.argmax(h, axis=1)",
+     "(h.shape[1] - 1 - np.argmax(h[:, ::-1], axis=1))"),
+    ("size-policy scalars swapped", "out[b, 0] = depth[b]\n            out[b, 1] = ctx_len[b]",
+     "out[b, 0] = ctx_len[b]\n            out[b, 1] = depth[b]"),
+    ("depth window misses the newest score", "out[b, n_feat - k:n_feat] = scores[b, n - k:n]",
+     "out[b, n_feat - k:n_feat] = scores[b, max(n - k - 1, 0):max(n - 1, k)]"),
+]
+
+
+def test_unmutated_policy_oracle_passes_every_pin():
+    for pin in POLICY_PINS:
+        pin()
+
+
+@pytest.mark.parametrize("idx", range(len(POLICY_MUTANTS)), ids=[m[0] for m in POLICY_MUTANTS])
+def test_every_policy_mutant_is_caught(idx, tmp_path, monkeypatch):
+    name, orig, mutated = POLICY_MUTANTS[idx]
+    src = open(_policy.__file__).read()
+    assert src.count(orig) >= 1, f"mutation anchor not found: {orig!r}"
+    path = tmp_path / f"policy_mutant{idx}.py"
+    path.write_text(src.replace(orig, mutated, 1))
+    spec = importlib.util.spec_from_file_location(f"policy_mutant{idx}", str(path))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    monkeypatch.setattr(TP, "OP", mod)
+    caught = False
+    for pin in POLICY_PINS:
+        try:
+            pin()
+        except (AssertionError, ValueError, IndexError):
+            caught = True
+            break
+    assert caught, f"pins did not notice: {name}"
