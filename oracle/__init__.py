@@ -55,6 +55,8 @@ def load_library(path: str) -> ctypes.CDLL:
     lib.ltd_oracle_kv_compact.restype = i32
     lib.ltd_oracle_select_candidates.argtypes = [P, P, P, P, P, i32, i32, i32, P, P, P, P, P]
     lib.ltd_oracle_select_candidates.restype = i32
+    lib.ltd_oracle_draft_expand.argtypes = [P, P, i32, i32, i32, i32, i32, P, P, P, P, i32, P]
+    lib.ltd_oracle_draft_expand.restype = i32
     lib.ltd_oracle_num_threads.argtypes = []
     lib.ltd_oracle_num_threads.restype = i32
     return lib
@@ -192,3 +194,24 @@ def select_candidates(scores, pool_parents, pool_tokens, pool_size, n_select, Nm
     if rc != 0:
         raise OracleError(rc)
     return (*outs, n_nodes)
+
+
+def draft_expand(logits, frontier, scores, pool_parents, pool_tokens, pool_size, *, W, W_next):
+    """One round of draft tree expansion (section 3.2, "Draft Tree
+    Generation"), in place on copies of the pool arrays.  Returns (scores,
+    pool_parents, pool_tokens, pool_size, new_frontier)."""
+    logits = np.ascontiguousarray(logits, np.float32)
+    B, F, Voc = logits.shape
+    frontier = np.ascontiguousarray(frontier, np.int32)
+    scores = np.array(scores, np.float32, copy=True)
+    pool_parents = np.array(pool_parents, np.int32, copy=True)
+    pool_tokens = np.array(pool_tokens, np.int32, copy=True)
+    pool_size = np.array(pool_size, np.int32, copy=True)
+    Vpool = scores.shape[1]
+    new_frontier = np.full((B, W_next), -1, np.int32)
+    rc = _load().ltd_oracle_draft_expand(
+        _ptr(logits), _ptr(frontier), B, F, Voc, W, W_next, _ptr(scores), _ptr(pool_parents),
+        _ptr(pool_tokens), _ptr(pool_size), Vpool, _ptr(new_frontier))
+    if rc != 0:
+        raise OracleError(rc)
+    return scores, pool_parents, pool_tokens, pool_size, new_frontier

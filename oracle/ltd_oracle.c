@@ -23,6 +23,11 @@
  *   selection        paper section 3.2 ("Candidate Token Selection"): of the
  *                    draft tree's candidates, the V with the highest predicted
  *                    (cumulative path) probability are kept and flattened.
+ *   expansion        paper section 3.2 ("Draft Tree Generation"): each leaf
+ *                    of the current level gets the W most probable tokens of
+ *                    its draft distribution as children; of all children, the
+ *                    W with the highest cumulative path probability become
+ *                    the next leaves.
  *
  * Readings of points the paper leaves open (softmax scale, node order, whether
  * V counts the root, tie rules, where tree K/V live) are fixed by the caller's
@@ -425,5 +430,69 @@ int ltd_oracle_select_candidates(const float* scores, const int32_t* pool_parent
   free(c);
   free(dep);
   free(new_id);
+  return 0;
+}
+
+/* ---- one round of draft tree expansion (section 3.2, "Draft Tree
+ * Generation").  For frontier node f of sequence b, with draft logits l over
+ * the vocabulary: log p(v) = l_v - log(sum_u exp(l_u)) (in double); its W
+ * children are the W tokens of largest logit (equal logits: lower token
+ * index first), in that order, and a child's score is its parent's score plus
+ * log p(token), stored as float.  Children are appended to the pool frontier
+ * by frontier; then the W_next children of highest stored score (equal
+ * scores: lower pool index first) become the next frontier, in that order. */
+int ltd_oracle_draft_expand(const float* logits, const int32_t* frontier, int B, int F, int Voc,
+                            int W, int W_next, float* scores, int32_t* pool_parents,
+                            int32_t* pool_tokens, int32_t* pool_size, int Vpool,
+                            int32_t* new_frontier) {
+  if (B < 0 || F < 1 || Voc < 1 || W < 1 || W > Voc || W_next < 1 || W_next > F * W || Vpool < 1)
+    return LTDO_EINVAL;
+  for (int b = 0; b < B; ++b) {
+    if (pool_size[b] < 1 || pool_size[b] + F * W > Vpool) return LTDO_STATUS_BAD_NNODES;
+    for (int f = 0; f < F; ++f)
+      if (frontier[(int64_t)b * F + f] < 0 || frontier[(int64_t)b * F + f] >= pool_size[b])
+        return LTDO_STATUS_BAD_PARENT;
+  }
+  const size_t n_taken = (size_t)(F * W > Voc ? F * W : Voc);
+  unsigned char* taken = (unsigned char*)malloc(n_taken);
+  if (!taken) return LTDO_EINVAL;
+  for (int b = 0; b < B; ++b) {
+    const int64_t pb = (int64_t)b * Vpool;
+    const int first = pool_size[b];
+    for (int f = 0; f < F; ++f) {
+      const float* row = logits + ((int64_t)b * F + f) * Voc;
+      const int parent = frontier[(int64_t)b * F + f];
+      double m = -INFINITY;
+      for (int v = 0; v < Voc; ++v)
+        if (row[v] > m) m = row[v];
+      double z = 0.0;
+      for (int v = 0; v < Voc; ++v) z += exp((double)row[v] - m);
+      const double lse = m + log(z);
+      memset(taken, 0, (size_t)Voc);
+      for (int r = 0; r < W; ++r) {
+        /* the largest logit not taken yet, lowest index on ties */
+        int best = -1;
+        for (int v = 0; v < Voc; ++v)
+          if (!taken[v] && (best < 0 || row[v] > row[best])) best = v;
+        taken[best] = 1;
+        const int c = first + f * W + r;
+        pool_parents[pb + c] = parent;
+        pool_tokens[pb + c] = best;
+        scores[pb + c] = (float)((double)scores[pb + parent] + ((double)row[best] - lse));
+      }
+    }
+    /* beam: the W_next children of highest score */
+    const int n_children = F * W;
+    memset(taken, 0, n_taken);
+    for (int r = 0; r < W_next; ++r) {
+      int best = -1;
+      for (int c = 0; c < n_children; ++c)
+        if (!taken[c] && (best < 0 || scores[pb + first + c] > scores[pb + first + best])) best = c;
+      taken[best] = 1;
+      new_frontier[(int64_t)b * W_next + r] = first + best;
+    }
+    pool_size[b] = first + n_children;
+  }
+  free(taken);
   return 0;
 }

@@ -83,6 +83,21 @@ int ltd_oracle_select_candidates(const float* scores, const int32_t* pool_parent
                                  int32_t* selected, int32_t* parents, int32_t* tokens,
                                  int32_t* depth, int32_t* n_nodes);
 
+/* One round of draft tree expansion (paper section 3.2, "Draft Tree
+ * Generation").  logits [B][F][Voc]: draft logits at the F frontier nodes,
+ * whose pool indices are frontier [B][F].  Appends F*W children per sequence
+ * to the pool ([B][Vpool] scores, parents, tokens) at pool_size[b] onwards:
+ * for each frontier node in order, its W tokens of largest logit (equal
+ * logits: lower token index first), each scored parent score + log-softmax
+ * of its logit (double, stored as float).  Then new_frontier [B][W_next] =
+ * the W_next new children of highest score (equal: lower pool index first),
+ * best first, and pool_size[b] += F*W.  Returns a status code when a pool
+ * would overflow or a frontier index is not in the pool. */
+int ltd_oracle_draft_expand(const float* logits, const int32_t* frontier, int B, int F, int Voc,
+                            int W, int W_next, float* scores, int32_t* pool_parents,
+                            int32_t* pool_tokens, int32_t* pool_size, int Vpool,
+                            int32_t* new_frontier);
+
 /* Threads the oracle's parallel loops use (OpenMP), for reporting. */
 int ltd_oracle_num_threads(void);
 

@@ -113,6 +113,10 @@ class DraftPool:
     tokens: np.ndarray  # int32 [n]
     scores: np.ndarray  # float64 [n] cumulative log-probability (root = 0)
     level: np.ndarray  # int32 [n] depth below the root
+    # every expansion, in order: (node, the W + 1 Dirichlet components sorted
+    # descending, the W child tokens); rounds of expansions are separated by
+    # the beam selection of the next leaves
+    draws: Optional[list] = None
 
 
 def _children_of(parents: np.ndarray) -> List[List[int]]:
@@ -144,10 +148,13 @@ def draft_pool(rng: np.random.Generator, depth: int, width: int, vocab: int) -> 
     pool_score = [0.0]
     pool_tok = [int(rng.integers(0, vocab))]
 
+    draws = []
+
     def expand(node: int) -> List[int]:
-        p = np.sort(rng.dirichlet(np.full(width + 1, 0.5)))[::-1][:width]
-        p = np.maximum(p, 1e-300)
+        full = np.sort(rng.dirichlet(np.full(width + 1, 0.5)))[::-1]
+        p = np.maximum(full[:width], 1e-300)
         toks = rng.choice(vocab, size=width, replace=False)
+        draws.append((node, full.copy(), toks.copy()))
         out = []
         for c in range(width):
             pool_par.append(node)
@@ -166,7 +173,7 @@ def draft_pool(rng: np.random.Generator, depth: int, width: int, vocab: int) -> 
             cand.sort(key=lambda j: -pool_score[j])
             leaves = cand[:width]
     return DraftPool(np.array(pool_par, np.int32), np.array(pool_tok, np.int32),
-                     np.array(pool_score, np.float64), np.array(pool_lvl, np.int32))
+                     np.array(pool_score, np.float64), np.array(pool_lvl, np.int32), draws)
 
 
 def tree_eagle(rng: np.random.Generator, n: int, depth: int, width: int, vocab: int) -> DraftTree:

@@ -12,6 +12,7 @@ import test_oracle_accept as TA
 import test_oracle_attention as TT
 import test_oracle_compact as TC
 import test_oracle_select as TS
+import test_oracle_expand as TE
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "ltd_oracle.c")
 
@@ -40,6 +41,12 @@ SELECT_PINS = [
     lambda: TS.test_matches_the_generators_own_selection(6, 10, 60),
     lambda: TS.test_star_pool_is_a_stable_argsort(),
     lambda: TS.test_validation_codes(),
+]
+
+EXPAND_PINS = [
+    lambda: TE.test_replays_the_generators_beam(4, 4, 50),
+    lambda: TE.test_matches_torch_log_softmax_topk(),
+    lambda: TE.test_ties(),
 ]
 
 # (name, original text, mutated text, pins expected to notice)
@@ -109,6 +116,23 @@ MUTANTS = [
      "const int V = n_select[b] <= pn ? n_select[b] - (n_select[b] > 1) : pn;", SELECT_PINS),
     ("depth not incremented", "dep[i] = i == 0 ? 0 : dep[par[i]] + 1;",
      "dep[i] = i == 0 ? 0 : dep[par[i]];", SELECT_PINS),
+    ("expansion scores the raw logit", "((double)row[best] - lse)", "((double)row[best])",
+     EXPAND_PINS),
+    ("expansion drops the parent's score", "(float)((double)scores[pb + parent] + ((double)row[best] - lse))",
+     "(float)((double)row[best] - lse)", EXPAND_PINS),
+    ("children are the least likely tokens", "if (!taken[v] && (best < 0 || row[v] > row[best])) best = v;",
+     "if (!taken[v] && (best < 0 || row[v] < row[best])) best = v;", EXPAND_PINS),
+    ("equal logits go to the higher token index",
+     "if (!taken[v] && (best < 0 || row[v] > row[best])) best = v;",
+     "if (!taken[v] && (best < 0 || row[v] >= row[best])) best = v;", EXPAND_PINS),
+    ("beam keeps the lowest scores",
+     "if (!taken[c] && (best < 0 || scores[pb + first + c] > scores[pb + first + best])) best = c;",
+     "if (!taken[c] && (best < 0 || scores[pb + first + c] < scores[pb + first + best])) best = c;",
+     EXPAND_PINS),
+    ("beam ties go to the higher pool index",
+     "if (!taken[c] && (best < 0 || scores[pb + first + c] > scores[pb + first + best])) best = c;",
+     "if (!taken[c] && (best < 0 || scores[pb + first + c] >= scores[pb + first + best])) best = c;",
+     EXPAND_PINS),
     ("a child scoring above its parent accepted",
      "if (i > 0 && sc[i] > sc[par[i]]) return LTDO_STATUS_BAD_SCORE;",
      "if (i > 0 && sc[i] > sc[par[i]] + 1.0f) return LTDO_STATUS_BAD_SCORE;", SELECT_PINS),
@@ -138,7 +162,7 @@ def _pins_pass(pins):
 
 
 def test_unmutated_oracle_passes_every_pin():
-    assert _pins_pass(ATTN_PINS + ACCEPT_PINS + COMPACT_PINS + SELECT_PINS)
+    assert _pins_pass(ATTN_PINS + ACCEPT_PINS + COMPACT_PINS + SELECT_PINS + EXPAND_PINS)
 
 
 @pytest.mark.parametrize("idx", range(len(MUTANTS)), ids=[m[0] for m in MUTANTS])
