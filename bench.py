@@ -15,7 +15,8 @@ over its average duration (a graph of K such calls, timed the same way).
 `cpu_baseline` times the CPU oracle on the host on a bounded sample.
 
 The steps before verification are timed apart the same way and reported
-under `kernels`, not in `value`: candidate selection (the V most probable
+under `kernels`, not in `value`: one draft expansion round (10 frontier nodes
+over the workload's vocabulary, `draft_expand`), candidate selection (the V most probable
 candidates of the draft pool flattened into the tree that is verified) on a
 pool of the workload's shape (`select_candidates`), and the size and depth
 policies' inference on one state per sequence (`size_policy`,
@@ -251,6 +252,36 @@ def main():
         "us": round(sel_us, 3), "workload": sb.label, "batch": sb.B,
         "pool": sb.pool_size.tolist()[:16], "V": sb.n_select.tolist()[:16],
         "outputs": "parents, tokens, n_nodes, selected", "in_value": False}
+
+    # ---- one draft expansion round, outside the step (a graph of K calls):
+    # W = 10 frontier nodes per sequence over the workload's vocabulary
+    rng = np.random.default_rng(2603)
+    e_logits = [to_dev((rng.standard_normal((b.B, 10, b.Voc)) * 2).astype(np.float32))
+                for _ in range(max(2, min(8, math.ceil(2.2 * MALL_BYTES / (b.B * 10 * b.Voc * 4)))))]
+    e_pool = [torch.zeros((b.B, 1024), dtype=torch.float32, device="cuda"),
+              torch.zeros((b.B, 1024), **i32), torch.zeros((b.B, 1024), **i32)]
+    e_size0 = torch.full((b.B,), 111, **i32)
+    e_size = torch.empty_like(e_size0)
+    e_front = torch.arange(1, 11, **i32).repeat(b.B, 1).contiguous()
+    e_next = torch.empty((b.B, 10), **i32)
+    e_ws = torch.empty(ltd.draft_expand_workspace_size(b.B, 10, b.Voc, 10), dtype=torch.uint8,
+                       device="cuda")
+
+    def expand(i):
+        e_size.copy_(e_size0)  # the round always appends at the same place
+        ltd.draft_expand(e_logits[i % len(e_logits)], e_front, *e_pool, e_size, e_next, W=10,
+                         workspace=e_ws, stream=stream)
+
+    torch.cuda.synchronize()
+    g = graph_of(expand, args.steps)
+    e_us = 1e3 * timed(lambda i: g.replay(), 1) / args.steps
+    del g
+    e_bytes = b.B * 10 * b.Voc * 4
+    kernels["draft_expand"] = {"us": round(e_us, 3), "batch": b.B, "frontier": 10, "W": 10,
+                               "vocab": b.Voc, "alg_bytes": e_bytes,
+                               "GB/s": round(e_bytes / (e_us * 1e-6) / 1e9, 1),
+                               "note": "includes a 4-byte device copy that resets the pool size",
+                               "in_value": False}
 
     # ---- draft policies, outside the step (graphs of K calls), one state
     # per sequence of the workload

@@ -21,8 +21,12 @@
  *                         paragraph: the remainder after the first error is
  *                         dropped).
  *
- * The step before it has a call of its own:
+ * The steps before it have calls of their own:
  *
+ *   ltd_draft_expand      one round of the draft tree's beam expansion
+ *                         (section 3.2, "Draft Tree Generation");
+ *   ltd_policy_forward    the size and depth policies' decisions (section 4,
+ *                         appendix A.2);
  *   ltd_select_candidates the V most probable candidates of the draft tree's
  *                         pool, flattened into the tree the three calls above
  *                         verify (section 3.2, "Candidate Token Selection").
@@ -77,6 +81,10 @@ extern "C" {
 
 #define LTD_MAX_NODES 256 /* largest Nmax (the paper's size policy spans V in [20, 240]) */
 #define LTD_MAX_POOL 1024 /* largest draft pool (1 + W + (D-2) W^2 = 1011 at W = 10, D = 12) */
+
+#define LTD_EXPAND_MAX_W 16          /* children per frontier node (the paper's W is 10) */
+#define LTD_EXPAND_MAX_CHUNKS 64     /* vocabulary up to 64 * 4096 = 262144 entries */
+#define LTD_EXPAND_MAX_CHILDREN 256  /* F * W per round */
 
 #define LTD_POLICY_SIZE 0          /* state [D, L, score of every pool candidate, pad ...] */
 #define LTD_POLICY_DEPTH 1         /* state [scores of the newest in_dim-2 candidates, D, L] */
@@ -225,6 +233,40 @@ int ltd_select_candidates(const float* scores, const int32_t* pool_parents,
                           const int32_t* n_select, int B, int Vpool, int Nmax, int32_t* selected,
                           int32_t* parents, int32_t* tokens, int32_t* depth, int32_t* n_nodes,
                           int validate, int32_t* status, void* stream);
+
+/*
+ * One round of draft tree expansion (section 3.2, "Draft Tree Generation":
+ * each leaf gets the W most probable tokens of its draft distribution as
+ * children; the W children of highest cumulative path probability become the
+ * next leaves).  The draft model's logits at the F frontier nodes are the
+ * input; the children are appended to the candidate pool that
+ * ltd_select_candidates and the policies read.
+ *
+ *   logits        [B][F][Voc] float32: draft logits at frontier node f.
+ *   frontier      [B][F] int32: the frontier nodes' pool indices.
+ *   scores, pool_parents, pool_tokens  [B][Vpool]: the pool, appended to.
+ *   pool_size     [B] int32: read, then advanced by F*W.
+ *   new_frontier  [B][W_next] int32: the next frontier (pool indices).
+ * For frontier node f, in order, its children are the W tokens of largest
+ * logit (equal logits: lower token index first), stored at pool_size + f*W
+ * + r with parent frontier[f] and score = parent's score + log-softmax of the
+ * logit (float32; the log-sum-exp is accumulated in double).  new_frontier
+ * is the W_next new children of highest score, best first (equal scores:
+ * lower pool index first).  A first round from the root has F = 1; after
+ * D - 1 rounds of width W the pool holds 1 + W + (D-2) W^2 candidates.
+ * Limits: 1 <= W <= LTD_EXPAND_MAX_W, W <= Voc <= 4096 * LTD_EXPAND_MAX_CHUNKS,
+ * 1 <= F*W <= LTD_EXPAND_MAX_CHILDREN, 1 <= W_next <= F*W.
+ * workspace: ltd_draft_expand_workspace_size(B, F, Voc, W) bytes.
+ * With validate != 0: LTD_STATUS_BAD_NNODES if pool_size[b] < 1 or the
+ * children would pass Vpool, LTD_STATUS_BAD_PARENT if a frontier index is
+ * not in the pool; then nothing is written.
+ */
+size_t ltd_draft_expand_workspace_size(int B, int F, int Voc, int W);
+
+int ltd_draft_expand(const float* logits, const int32_t* frontier, int B, int F, int Voc, int W,
+                     int W_next, float* scores, int32_t* pool_parents, int32_t* pool_tokens,
+                     int32_t* pool_size, int Vpool, int32_t* new_frontier, void* workspace,
+                     size_t workspace_bytes, int validate, int32_t* status, void* stream);
 
 /*
  * Draft-policy inference (section 4: the state vector of draft depth D,

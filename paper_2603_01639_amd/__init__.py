@@ -50,6 +50,8 @@ EXPORTED = (
     "ltd_select_candidates",
     "ltd_policy_workspace_size",
     "ltd_policy_forward",
+    "ltd_draft_expand_workspace_size",
+    "ltd_draft_expand",
 )
 
 
@@ -91,6 +93,10 @@ def lib() -> ctypes.CDLL:
         L.ltd_policy_forward.argtypes = ([i32, P, P, i32, P, P, f32, i32, i32, P, P, i32, P, P, i32,
                                           P, P, i32, i32, i32, P, P, P, sz, P])
         L.ltd_policy_forward.restype = i32
+        L.ltd_draft_expand_workspace_size.argtypes = [i32] * 4
+        L.ltd_draft_expand_workspace_size.restype = sz
+        L.ltd_draft_expand.argtypes = [P, P] + [i32] * 5 + [P] * 4 + [i32, P, P, sz, i32, P, P]
+        L.ltd_draft_expand.restype = i32
         L.ltd_version.argtypes = []
         L.ltd_version.restype = ctypes.c_char_p
         _lib = L
@@ -242,3 +248,23 @@ def policy_forward(layout, scores, pool_size, depth, ctx_len, layers, logits, ac
         int(action_offset), int(action_scale), _p(logits), _p(action), _p(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream))
     _check("ltd_policy_forward", rc)
+
+
+def draft_expand_workspace_size(B, F, Voc, W) -> int:
+    return int(lib().ltd_draft_expand_workspace_size(B, F, Voc, W))
+
+
+def draft_expand(logits, frontier, scores, pool_parents, pool_tokens, pool_size, new_frontier, *,
+                 W: int, workspace=None, validate: bool = False, status=None, stream=None):
+    """One round of draft tree expansion; see ``ltd_draft_expand``.  logits
+    ``[B][F][Voc]`` float32, pool arrays ``[B][Vpool]`` (updated in place),
+    new_frontier ``[B][W_next]``."""
+    B, F, Voc = logits.shape
+    Vpool = scores.shape[1]
+    if workspace is None:
+        workspace = _alloc_workspace(draft_expand_workspace_size(B, F, Voc, W), logits.device)
+    rc = lib().ltd_draft_expand(
+        _p(logits), _p(frontier), B, F, Voc, int(W), new_frontier.shape[1], _p(scores),
+        _p(pool_parents), _p(pool_tokens), _p(pool_size), Vpool, _p(new_frontier), _p(workspace),
+        workspace.numel() * workspace.element_size(), int(validate), _p(status), _stream(stream))
+    _check("ltd_draft_expand", rc)

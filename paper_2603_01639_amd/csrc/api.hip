@@ -187,6 +187,39 @@ int ltd_select_candidates(const float* scores, const int32_t* pool_parents,
   return LTD_OK;
 }
 
+namespace {
+bool expand_args_ok(int B, int F, int Voc, int W) {
+  return B >= 0 && F >= 1 && W >= 1 && W <= LTD_EXPAND_MAX_W && Voc >= W &&
+         ltd::expand_chunks(Voc) <= LTD_EXPAND_MAX_CHUNKS && F * W <= LTD_EXPAND_MAX_CHILDREN;
+}
+}  // namespace
+
+size_t ltd_draft_expand_workspace_size(int B, int F, int Voc, int W) {
+  if (!expand_args_ok(B, F, Voc, W)) return 0;
+  return ltd::expand_workspace_bytes(B, F, Voc, W);
+}
+
+int ltd_draft_expand(const float* logits, const int32_t* frontier, int B, int F, int Voc, int W,
+                     int W_next, float* scores, int32_t* pool_parents, int32_t* pool_tokens,
+                     int32_t* pool_size, int Vpool, int32_t* new_frontier, void* workspace,
+                     size_t workspace_bytes, int validate, int32_t* status, void* stream) {
+  if (Voc < 1 || F < 1 || W < 1 || F > LTD_EXPAND_MAX_CHILDREN || !expand_args_ok(B, F, Voc, W) ||
+      W_next < 1 || W_next > F * W || Vpool < 1)
+    return LTD_EINVAL;
+  if (validate && !status) return LTD_EINVAL;
+  if (B == 0) return LTD_OK;
+  if (!logits || !frontier || !scores || !pool_parents || !pool_tokens || !pool_size ||
+      !new_frontier)
+    return LTD_EINVAL;
+  if (!workspace || workspace_bytes < ltd::expand_workspace_bytes(B, F, Voc, W))
+    return LTD_EWORKSPACE;
+  if (ltd::launch_expand(logits, frontier, B, F, Voc, W, W_next, scores, pool_parents,
+                         pool_tokens, pool_size, Vpool, new_frontier, workspace, status,
+                         validate != 0, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return LTD_EHIP;
+  return LTD_OK;
+}
+
 size_t ltd_policy_workspace_size(int B, int h1, int h2) {
   if (B < 0 || h1 < 1 || h1 > LTD_POLICY_MAX_HIDDEN || h2 < 0 || h2 > LTD_POLICY_MAX_HIDDEN)
     return 0;

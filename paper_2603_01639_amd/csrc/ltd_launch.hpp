@@ -66,6 +66,15 @@ hipError_t launch_select(const float* scores, const int32_t* pool_parents,
                          int32_t* parents, int32_t* tokens, int32_t* depth, int32_t* n_nodes,
                          const int32_t* status, hipStream_t stream);
 
+// expand.hip
+int expand_chunks(int Voc);
+size_t expand_workspace_bytes(int B, int F, int Voc, int W);
+hipError_t launch_expand(const float* logits, const int32_t* frontier, int B, int F, int Voc,
+                         int W, int W_next, float* scores, int32_t* pool_parents,
+                         int32_t* pool_tokens, int32_t* pool_size, int Vpool,
+                         int32_t* new_frontier, void* workspace, int32_t* status, bool validate,
+                         hipStream_t stream);
+
 // policy.hip
 size_t policy_workspace_bytes(int B, int h1, int h2);
 hipError_t launch_policy(int layout, const float* scores, const int32_t* pool_size, int Vpool,

@@ -58,28 +58,6 @@ struct PoolInput {
   float pad;
 };
 
-// Lane exchanges for the butterflies (wave64, lane layouts of gfx950's
-// permlane swaps and DPP row rotations):
-//   xor 32 / xor 16: v_permlane{32,16}_swap of (a, b) hands lane l the value
-//     of b (lower half of the pair) or a (upper half) from its partner;
-//   xor 8: row_ror:8; xor 4: row_ror:4 for lanes with bit 2 set, row_ror:12
-//     otherwise; xor 2 / xor 1: quad_perm [2,3,0,1] / [1,0,3,2].
-template <int kCtrl>
-__device__ __forceinline__ float dpp_f(float v) {
-  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kCtrl, 0xF, 0xF, false));
-}
-template <int kDist>
-__device__ __forceinline__ float xor_lane(float v, int lane) {
-  if constexpr (kDist == 8) return dpp_f<0x128>(v);
-  if constexpr (kDist == 4) {
-    const float a = dpp_f<0x124>(v);
-    const float b = dpp_f<0x12C>(v);
-    return (lane & 4) ? a : b;
-  }
-  if constexpr (kDist == 2) return dpp_f<0x4E>(v);
-  return dpp_f<0xB1>(v);
-}
-
 // One halving level of the butterfly at distance `dist`: lanes with that bit
 // set keep the upper half of the partial sums, the others the lower half, and
 // each adds its partner's copy of what it keeps.
@@ -100,7 +78,7 @@ __device__ __forceinline__ void halve(float* acc, int lane) {
         from_partner = __uint_as_float(upper ? r[0] : r[1]);
       }
     } else {
-      from_partner = xor_lane<kDist>(upper ? acc[q] : acc[q + kHalf], lane);
+      from_partner = lane_xor_f<kDist>(upper ? acc[q] : acc[q + kHalf], lane);
     }
     acc[q] = (upper ? acc[q + kHalf] : acc[q]) + from_partner;
   }
@@ -108,16 +86,12 @@ __device__ __forceinline__ void halve(float* acc, int lane) {
 
 // Sum of v over all 64 lanes, in every lane.
 __device__ __forceinline__ float wave_total(float v, int lane) {
-  v += __uint_as_float(
-      __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false)[
-          (lane & 32) ? 0 : 1]);
-  v += __uint_as_float(
-      __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false)[
-          (lane & 16) ? 0 : 1]);
-  v += xor_lane<8>(v, lane);
-  v += xor_lane<4>(v, lane);
-  v += xor_lane<2>(v, lane);
-  v += xor_lane<1>(v, lane);
+  v += lane_xor_f<32>(v, lane);
+  v += lane_xor_f<16>(v, lane);
+  v += lane_xor_f<8>(v, lane);
+  v += lane_xor_f<4>(v, lane);
+  v += lane_xor_f<2>(v, lane);
+  v += lane_xor_f<1>(v, lane);
   return v;
 }
 
@@ -243,18 +217,12 @@ __global__ void __launch_bounds__(kThreads) dense_kernel(const float* __restrict
     if constexpr (kLevels >= 3) halve<kStates / 8, 8>(acc, lane);
     if constexpr (kLevels >= 4) halve<kStates / 16, 4>(acc, lane);
     float r = acc[0];
-    if constexpr (kLevels < 1)
-      r += __uint_as_float(__builtin_amdgcn_permlane32_swap(__float_as_uint(r),
-                                                           __float_as_uint(r), false,
-                                                           false)[(lane & 32) ? 0 : 1]);
-    if constexpr (kLevels < 2)
-      r += __uint_as_float(__builtin_amdgcn_permlane16_swap(__float_as_uint(r),
-                                                           __float_as_uint(r), false,
-                                                           false)[(lane & 16) ? 0 : 1]);
-    if constexpr (kLevels < 3) r += xor_lane<8>(r, lane);
-    if constexpr (kLevels < 4) r += xor_lane<4>(r, lane);
-    r += xor_lane<2>(r, lane);
-    r += xor_lane<1>(r, lane);
+    if constexpr (kLevels < 1) r += lane_xor_f<32>(r, lane);
+    if constexpr (kLevels < 2) r += lane_xor_f<16>(r, lane);
+    if constexpr (kLevels < 3) r += lane_xor_f<8>(r, lane);
+    if constexpr (kLevels < 4) r += lane_xor_f<4>(r, lane);
+    r += lane_xor_f<2>(r, lane);
+    r += lane_xor_f<1>(r, lane);
     constexpr int kGroupBits = 6 - kLevels;
     const int b = b0 + (lane >> kGroupBits);
     if (active && (lane & ((1 << kGroupBits) - 1)) == 0 && b < B)

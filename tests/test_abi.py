@@ -142,3 +142,18 @@ def test_policy_workspace_and_missing_buffers():
                                         P, 2, 0, 1, P, P, P, 1 << 20, None) == ltd.LTD_EINVAL
     assert ltd.lib().ltd_policy_forward(0, P, P, 16, P, P, 0.0, 1, 10, P, P, 8, P, P, 4, P, P, 2,
                                         0, 1, P, P, P, 4, None) == ltd.LTD_EWORKSPACE
+
+
+@pytest.mark.parametrize("B,F,Voc,W,W_next", [
+    (-1, 1, 100, 4, 4), (1, 0, 100, 4, 4), (1, 1, 100, 0, 1), (1, 1, 100, 17, 4), (1, 1, 3, 4, 4),
+    (1, 1, 64 * 4096 + 1, 4, 4), (1, 17, 100, 16, 4), (1, 2, 100, 4, 9), (1, 2, 100, 4, 0)])
+def test_draft_expand_rejects_bad_scalar_arguments(B, F, Voc, W, W_next):
+    P = 0x1000
+    rc = ltd.lib().ltd_draft_expand(P, P, B, F, Voc, W, W_next, P, P, P, P, 64, P, P, 1 << 30, 0,
+                                    None, None)
+    assert rc == ltd.LTD_EINVAL
+
+
+def test_draft_expand_workspace():
+    assert ltd.draft_expand_workspace_size(2, 10, 128256, 10) == 2 * 10 * 32 * (8 * 10 + 8)
+    assert ltd.draft_expand_workspace_size(1, 1, 64 * 4096 + 1, 4) == 0
