@@ -57,6 +57,9 @@ def load_library(path: str) -> ctypes.CDLL:
     lib.ltd_oracle_select_candidates.restype = i32
     lib.ltd_oracle_draft_expand.argtypes = [P, P, i32, i32, i32, i32, i32, P, P, P, P, i32, P]
     lib.ltd_oracle_draft_expand.restype = i32
+    lib.ltd_oracle_tree_accept_sampling.argtypes = [P, P, P, P, P, P, i32, i32, i32, ctypes.c_double,
+                                                     P, P, P, P, P]
+    lib.ltd_oracle_tree_accept_sampling.restype = i32
     lib.ltd_oracle_num_threads.argtypes = []
     lib.ltd_oracle_num_threads.restype = i32
     return lib
@@ -215,3 +218,29 @@ def draft_expand(logits, frontier, scores, pool_parents, pool_tokens, pool_size,
     if rc != 0:
         raise OracleError(rc)
     return scores, pool_parents, pool_tokens, pool_size, new_frontier
+
+
+def tree_accept_sampling(logits, draft_probs, draft_tokens, parents, n_nodes, uniforms, *,
+                         temperature=1.0, want_final=False):
+    """Acceptance by recursive rejection sampling at temperature T > 0.
+    Returns (accepted_nodes, out_tokens, n_accepted, min_margin) and, with
+    want_final, the distribution each bonus token was drawn from."""
+    logits = np.ascontiguousarray(logits, np.float32)
+    B, Nmax, Voc = logits.shape
+    draft_probs = np.ascontiguousarray(draft_probs, np.float32)
+    draft_tokens = np.ascontiguousarray(draft_tokens, np.int32)
+    parents = np.ascontiguousarray(parents, np.int32)
+    n_nodes = np.ascontiguousarray(n_nodes, np.int32)
+    uniforms = np.ascontiguousarray(uniforms, np.float32)
+    acc = np.full((B, Nmax), -1, np.int32)
+    toks = np.full((B, Nmax), -1, np.int32)
+    n_acc = np.zeros(B, np.int32)
+    margin = np.zeros(B, np.float64)
+    final = np.zeros((B, Voc), np.float64) if want_final else None
+    rc = _load().ltd_oracle_tree_accept_sampling(
+        _ptr(logits), _ptr(draft_probs), _ptr(draft_tokens), _ptr(parents), _ptr(n_nodes),
+        _ptr(uniforms), B, Nmax, Voc, float(temperature), _ptr(acc), _ptr(toks), _ptr(n_acc),
+        _ptr(final), _ptr(margin))
+    if rc != 0:
+        raise OracleError(rc)
+    return (acc, toks, n_acc, margin, final) if want_final else (acc, toks, n_acc, margin)

@@ -23,6 +23,12 @@
  *   selection        paper section 3.2 ("Candidate Token Selection"): of the
  *                    draft tree's candidates, the V with the highest predicted
  *                    (cumulative path) probability are kept and flattened.
+ *   sampling         acceptance at temperature T > 0, the paper's second
+ *                    setting (its experiments report T = 0 and T = 1; the rule
+ *                    is the one its baseline inherits, not printed in the
+ *                    paper): recursive rejection sampling over each node's
+ *                    children, which were drawn without replacement from the
+ *                    draft distribution.
  *   expansion        paper section 3.2 ("Draft Tree Generation"): each leaf
  *                    of the current level gets the W most probable tokens of
  *                    its draft distribution as children; of all children, the
@@ -494,5 +500,132 @@ int ltd_oracle_draft_expand(const float* logits, const int32_t* frontier, int B,
     pool_size[b] = first + n_children;
   }
   free(taken);
+  return 0;
+}
+
+/* ---- acceptance by recursive rejection sampling at temperature T > 0.
+ * Written as the literal recursion over explicit distributions, in double.
+ * At node u the target distribution is P = softmax(logits[u] / T) and the
+ * draft distribution Q = draft_probs[u] / sum(draft_probs[u]).  Children are
+ * tried in ascending node index (the order they were drawn).  Child c with
+ * token x is accepted when uniforms[c][0] * Q(x) < P(x) (probability
+ * min(1, P(x)/Q(x))); the walk then continues at c.  On rejection, P becomes
+ * max(P - Q, 0) renormalised (unchanged if that has no mass) and Q loses x
+ * and is renormalised.  When no child is accepted (or u is a leaf) the bonus
+ * token is drawn from the current P by inverse CDF at uniforms[u][1]: the
+ * smallest v whose cumulative mass exceeds uniforms[u][1] * sum(P) (the last
+ * v with mass if rounding leaves none).  Optional outputs: final_dist [B][Voc]
+ * (the distribution the bonus was drawn from) and min_margin [B] (the
+ * smallest |r Q(x) - P(x)| / max(P(x), r Q(x)) over the accept tests taken). */
+int ltd_oracle_tree_accept_sampling(const float* logits, const float* draft_probs,
+                                    const int32_t* draft_tokens, const int32_t* parents,
+                                    const int32_t* n_nodes, const float* uniforms, int B, int Nmax,
+                                    int Voc, double temperature, int32_t* accepted_nodes,
+                                    int32_t* out_tokens, int32_t* n_accepted, double* final_dist,
+                                    double* min_margin) {
+  if (B < 0 || Nmax < 1 || Voc < 1 || !(temperature > 0.0)) return LTDO_EINVAL;
+  for (int b = 0; b < B; ++b) {
+    const int n = n_nodes[b];
+    if (n < 1 || n > Nmax) return LTDO_STATUS_BAD_NNODES;
+    const int32_t* par = parents + (int64_t)b * Nmax;
+    if (par[0] != -1) return LTDO_STATUS_BAD_PARENT;
+    for (int i = 1; i < n; ++i)
+      if (par[i] < 0 || par[i] >= i) return LTDO_STATUS_BAD_PARENT;
+  }
+  double* P = (double*)malloc(sizeof(double) * (size_t)Voc);
+  double* Q = (double*)malloc(sizeof(double) * (size_t)Voc);
+  if (!P || !Q) {
+    free(P);
+    free(Q);
+    return LTDO_EINVAL;
+  }
+  for (int b = 0; b < B; ++b) {
+    const int n = n_nodes[b];
+    const int32_t* par = parents + (int64_t)b * Nmax;
+    const int32_t* tok = draft_tokens + (int64_t)b * Nmax;
+    const float* ur = uniforms + (int64_t)b * Nmax * 2;
+    int32_t* path = accepted_nodes + (int64_t)b * Nmax;
+    int32_t* ot = out_tokens + (int64_t)b * Nmax;
+    double margin = INFINITY;
+    int len = 0;
+    int u = 0;
+    path[len++] = 0;
+    for (;;) {
+      const float* lu = logits + ((int64_t)b * Nmax + u) * Voc;
+      double m = -INFINITY;
+      for (int v = 0; v < Voc; ++v)
+        if (lu[v] > m) m = lu[v];
+      double z = 0.0;
+      for (int v = 0; v < Voc; ++v) {
+        P[v] = exp(((double)lu[v] - m) / temperature);
+        z += P[v];
+      }
+      for (int v = 0; v < Voc; ++v) P[v] /= z;
+      int has_child = 0;
+      for (int c = u + 1; c < n; ++c)
+        if (par[c] == u) has_child = 1;
+      if (has_child) {
+        const float* qu = draft_probs + ((int64_t)b * Nmax + u) * Voc;
+        double qs = 0.0;
+        for (int v = 0; v < Voc; ++v) qs += qu[v];
+        for (int v = 0; v < Voc; ++v) Q[v] = qu[v] / qs;
+      }
+      int next = -1;
+      for (int c = u + 1; c < n && next < 0; ++c) {
+        if (par[c] != u) continue;
+        const int x = tok[c];
+        const double r = ur[2 * c];
+        const double lhs = r * Q[x];
+        const double den = lhs > P[x] ? lhs : P[x];
+        if (den > 0) {
+          const double mg = fabs(lhs - P[x]) / den;
+          if (mg < margin) margin = mg;
+        }
+        if (lhs < P[x]) {
+          next = c;
+          break;
+        }
+        /* rejected: residual target, draft without x */
+        double s = 0.0;
+        for (int v = 0; v < Voc; ++v) s += P[v] > Q[v] ? P[v] - Q[v] : 0.0;
+        if (s > 0.0)
+          for (int v = 0; v < Voc; ++v) P[v] = (P[v] > Q[v] ? P[v] - Q[v] : 0.0) / s;
+        Q[x] = 0.0;
+        double qs = 0.0;
+        for (int v = 0; v < Voc; ++v) qs += Q[v];
+        if (qs > 0.0)
+          for (int v = 0; v < Voc; ++v) Q[v] /= qs;
+      }
+      if (next >= 0) {
+        path[len++] = next;
+        u = next;
+        continue;
+      }
+      /* bonus token from P by inverse CDF */
+      double total = 0.0;
+      for (int v = 0; v < Voc; ++v) total += P[v];
+      const double target = (double)ur[2 * u + 1] * total;
+      int bonus = -1, last = 0;
+      double cum = 0.0;
+      for (int v = 0; v < Voc; ++v) {
+        if (P[v] > 0.0) last = v;
+        cum += P[v];
+        if (cum > target && P[v] > 0.0) {
+          bonus = v;
+          break;
+        }
+      }
+      if (bonus < 0) bonus = last;
+      for (int j = 1; j < len; ++j) ot[j - 1] = tok[path[j]];
+      ot[len - 1] = bonus;
+      if (final_dist)
+        for (int v = 0; v < Voc; ++v) final_dist[(int64_t)b * Voc + v] = P[v];
+      break;
+    }
+    n_accepted[b] = len;
+    if (min_margin) min_margin[b] = margin;
+  }
+  free(P);
+  free(Q);
   return 0;
 }

@@ -83,6 +83,22 @@ int ltd_oracle_select_candidates(const float* scores, const int32_t* pool_parent
                                  int32_t* selected, int32_t* parents, int32_t* tokens,
                                  int32_t* depth, int32_t* n_nodes);
 
+/* Acceptance by recursive rejection sampling at temperature T > 0 (the
+ * paper's T = 1 setting; the rule is the baseline's, not printed in the
+ * paper).  Same tree arguments and path/token outputs as
+ * ltd_oracle_tree_accept; draft_probs [B][Nmax][Voc] holds, for every node
+ * with children, the draft distribution its children were drawn from
+ * (without replacement, in ascending node order); uniforms [B][Nmax][2] in
+ * [0, 1): [c][0] decides child c, [u][1] the bonus token drawn at u.  Optional
+ * final_dist [B][Voc] receives the distribution the bonus was drawn from and
+ * min_margin [B] the smallest relative gap of an accept test. */
+int ltd_oracle_tree_accept_sampling(const float* logits, const float* draft_probs,
+                                    const int32_t* draft_tokens, const int32_t* parents,
+                                    const int32_t* n_nodes, const float* uniforms, int B, int Nmax,
+                                    int Voc, double temperature, int32_t* accepted_nodes,
+                                    int32_t* out_tokens, int32_t* n_accepted, double* final_dist,
+                                    double* min_margin);
+
 /* One round of draft tree expansion (paper section 3.2, "Draft Tree
  * Generation").  logits [B][F][Voc]: draft logits at the F frontier nodes,
  * whose pool indices are frontier [B][F].  Appends F*W children per sequence

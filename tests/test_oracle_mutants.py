@@ -13,6 +13,7 @@ import test_oracle_attention as TT
 import test_oracle_compact as TC
 import test_oracle_select as TS
 import test_oracle_expand as TE
+import test_oracle_sampling as TSa
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "ltd_oracle.c")
 
@@ -47,6 +48,13 @@ EXPAND_PINS = [
     lambda: TE.test_replays_the_generators_beam(4, 4, 50),
     lambda: TE.test_matches_torch_log_softmax_topk(),
     lambda: TE.test_ties(),
+]
+
+SAMPLING_PINS = [
+    lambda: TSa.test_worked_examples(),
+    lambda: TSa.test_losslessness_on_a_toy_model(),
+    lambda: TSa.test_draft_equal_to_target_accepts_the_first_child(),
+    lambda: TSa.test_lone_root_is_inverse_cdf_sampling(),
 ]
 
 # (name, original text, mutated text, pins expected to notice)
@@ -116,6 +124,20 @@ MUTANTS = [
      "const int V = n_select[b] <= pn ? n_select[b] - (n_select[b] > 1) : pn;", SELECT_PINS),
     ("depth not incremented", "dep[i] = i == 0 ? 0 : dep[par[i]] + 1;",
      "dep[i] = i == 0 ? 0 : dep[par[i]];", SELECT_PINS),
+    ("sampling: residual not renormalised",
+     "for (int v = 0; v < Voc; ++v) P[v] = (P[v] > Q[v] ? P[v] - Q[v] : 0.0) / s;",
+     "for (int v = 0; v < Voc; ++v) P[v] = (P[v] > Q[v] ? P[v] - Q[v] : 0.0);", SAMPLING_PINS),
+    ("sampling: draft keeps a rejected token", "        Q[x] = 0.0;\n", "\n", SAMPLING_PINS),
+    ("sampling: acceptance test inverted", "        if (lhs < P[x]) {", "        if (lhs > P[x]) {",
+     SAMPLING_PINS),
+    ("sampling: residual of the draft over the target",
+     "for (int v = 0; v < Voc; ++v) P[v] = (P[v] > Q[v] ? P[v] - Q[v] : 0.0) / s;",
+     "for (int v = 0; v < Voc; ++v) P[v] = (Q[v] > P[v] ? Q[v] - P[v] : 0.0) / s;", SAMPLING_PINS),
+    ("sampling: temperature ignored", "P[v] = exp(((double)lu[v] - m) / temperature);",
+     "P[v] = exp((double)lu[v] - m);", SAMPLING_PINS),
+    ("sampling: no residual after a rejection",
+     "        if (s > 0.0)\n          for (int v = 0; v < Voc; ++v) P[v] = (P[v] > Q[v] ? P[v] - Q[v] : 0.0) / s;",
+     "", SAMPLING_PINS),
     ("expansion scores the raw logit", "((double)row[best] - lse)", "((double)row[best])",
      EXPAND_PINS),
     ("expansion drops the parent's score", "(float)((double)scores[pb + parent] + ((double)row[best] - lse))",
@@ -162,7 +184,8 @@ def _pins_pass(pins):
 
 
 def test_unmutated_oracle_passes_every_pin():
-    assert _pins_pass(ATTN_PINS + ACCEPT_PINS + COMPACT_PINS + SELECT_PINS + EXPAND_PINS)
+    assert _pins_pass(ATTN_PINS + ACCEPT_PINS + COMPACT_PINS + SELECT_PINS + EXPAND_PINS +
+                      SAMPLING_PINS)
 
 
 @pytest.mark.parametrize("idx", range(len(MUTANTS)), ids=[m[0] for m in MUTANTS])
