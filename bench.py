@@ -15,7 +15,9 @@ over its average duration (a graph of K such calls, timed the same way).
 `cpu_baseline` times the CPU oracle on the host on a bounded sample.
 
 The steps before verification are timed apart the same way and reported
-under `kernels`, not in `value`: one draft expansion round (10 frontier nodes
+under `kernels`, not in `value`: acceptance at temperature 1 on the 8B-shaped
+tree (`tree_accept_sampling`, the alternative to greedy acceptance), one draft
+expansion round (10 frontier nodes
 over the workload's vocabulary, `draft_expand`), candidate selection (the V most probable
 candidates of the draft pool flattened into the tree that is verified) on a
 pool of the workload's shape (`select_candidates`), and the size and depth
@@ -282,6 +284,34 @@ def main():
                                "GB/s": round(e_bytes / (e_us * 1e-6) / 1e9, 1),
                                "note": "includes a 4-byte device copy that resets the pool size",
                                "in_value": False}
+
+    # ---- acceptance at T = 1 (recursive rejection sampling) on the 8B-shaped
+    # tree, in place of greedy acceptance (a graph of K calls)
+    from paper_2603_01639_amd import workloads as W
+    smp = W.sampling_8b(0)
+    s_in = [to_dev(a) for a in (smp.logits, smp.draft_probs, smp.draft_tokens, smp.parents,
+                                smp.n_nodes, smp.uniforms)]
+    s_acc = torch.empty((smp.B, smp.logits.shape[1]), **i32)
+    s_tok = torch.empty_like(s_acc)
+    s_n = torch.empty((smp.B,), **i32)
+    s_ws = torch.empty(ltd.accept_sampling_workspace_size(smp.B, smp.logits.shape[1],
+                                                          smp.logits.shape[2]),
+                       dtype=torch.uint8, device="cuda")
+
+    def sampling(i):
+        ltd.tree_accept_sampling(*s_in, s_acc, s_tok, s_n, temperature=smp.temperature,
+                                 workspace=s_ws, stream=stream)
+
+    torch.cuda.synchronize()
+    g = graph_of(sampling, args.steps)
+    s_us = 1e3 * timed(lambda i: g.replay(), 1) / args.steps
+    del g
+    s_nacc = int(s_n.cpu()[0])
+    kernels["tree_accept_sampling"] = {
+        "us": round(s_us, 3), "workload": smp.label, "n_accepted": s_nacc,
+        "note": "T = 1; the draft distributions and uniforms are inputs; cost grows with the "
+                "rejections on the accepted path (one vocabulary pass each)",
+        "in_value": False}
 
     # ---- draft policies, outside the step (graphs of K calls), one state
     # per sequence of the workload

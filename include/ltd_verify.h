@@ -82,6 +82,8 @@ extern "C" {
 #define LTD_MAX_NODES 256 /* largest Nmax (the paper's size policy spans V in [20, 240]) */
 #define LTD_MAX_POOL 1024 /* largest draft pool (1 + W + (D-2) W^2 = 1011 at W = 10, D = 12) */
 
+#define LTD_SAMPLING_MAX_CHUNKS 64  /* sampling vocabulary up to 64 * 4096 = 262144 entries */
+
 #define LTD_EXPAND_MAX_W 16          /* children per frontier node (the paper's W is 10) */
 #define LTD_EXPAND_MAX_CHUNKS 64     /* vocabulary up to 64 * 4096 = 262144 entries */
 #define LTD_EXPAND_MAX_CHILDREN 256  /* F * W per round */
@@ -159,6 +161,43 @@ int ltd_tree_accept(const float* logits, const int32_t* draft_tokens, const int3
                     int32_t* accepted_nodes, int32_t* out_tokens, int32_t* n_accepted,
                     void* workspace, size_t workspace_bytes, int validate, int32_t* status,
                     void* stream);
+
+/*
+ * Acceptance at temperature T > 0 (the paper's T = 1 setting; its rule is
+ * the baseline's, not printed in the paper): recursive rejection sampling
+ * over each node's children, which must have been drawn without replacement
+ * from the node's draft distribution, in ascending node order.
+ *
+ * At node u, with target P = softmax(logits[u] / T) and draft distribution
+ * Q = draft_probs[u] / sum(draft_probs[u]), child c (token x) is accepted
+ * when uniforms[c][0] * Q(x) < P(x), i.e. with probability min(1, P/Q), and
+ * the walk moves to c.  On rejection P becomes max(P - Q, 0) renormalised and
+ * Q drops x.  When no child is accepted (or u is a leaf) the bonus token is
+ * the inverse-CDF sample of P at uniforms[u][1].  The emitted tokens are then
+ * distributed exactly as the target's own sampling.
+ *
+ *   logits       [B][Nmax][Voc] float32, target logits at every node.
+ *   draft_probs  [B][Nmax][Voc] float32, read only for nodes with children
+ *                (non-negative, positive sum).
+ *   draft_tokens [B][Nmax] int32 in [0, Voc); siblings distinct.
+ *   uniforms     [B][Nmax][2] float32 in [0, 1).
+ *   temperature  finite and > 0, else LTD_EINVAL.
+ *   Outputs as ltd_tree_accept: accepted_nodes, out_tokens (the accepted
+ *   drafts, then the bonus), n_accepted.  Entries past n_accepted untouched.
+ *   Voc <= 4096 * LTD_SAMPLING_MAX_CHUNKS.
+ *   workspace: ltd_tree_accept_sampling_workspace_size(B, Nmax, Voc) bytes.
+ * Decisions are taken on float32 element arithmetic with double sums, so they
+ * can differ from an exact evaluation only where a uniform lies within about
+ * 1e-6 (relative) of its threshold.
+ */
+size_t ltd_tree_accept_sampling_workspace_size(int B, int Nmax, int Voc);
+
+int ltd_tree_accept_sampling(const float* logits, const float* draft_probs,
+                             const int32_t* draft_tokens, const int32_t* parents,
+                             const int32_t* n_nodes, const float* uniforms, int B, int Nmax,
+                             int Voc, float temperature, int32_t* accepted_nodes,
+                             int32_t* out_tokens, int32_t* n_accepted, void* workspace,
+                             size_t workspace_bytes, int validate, int32_t* status, void* stream);
 
 /*
  * KV compaction (the candidates after the first mismatch are discarded,

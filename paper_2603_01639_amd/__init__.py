@@ -52,6 +52,8 @@ EXPORTED = (
     "ltd_policy_forward",
     "ltd_draft_expand_workspace_size",
     "ltd_draft_expand",
+    "ltd_tree_accept_sampling_workspace_size",
+    "ltd_tree_accept_sampling",
 )
 
 
@@ -97,6 +99,11 @@ def lib() -> ctypes.CDLL:
         L.ltd_draft_expand_workspace_size.restype = sz
         L.ltd_draft_expand.argtypes = [P, P] + [i32] * 5 + [P] * 4 + [i32, P, P, sz, i32, P, P]
         L.ltd_draft_expand.restype = i32
+        L.ltd_tree_accept_sampling_workspace_size.argtypes = [i32] * 3
+        L.ltd_tree_accept_sampling_workspace_size.restype = sz
+        L.ltd_tree_accept_sampling.argtypes = [P] * 6 + [i32] * 3 + [f32] + [P] * 4 + [sz, i32, P,
+                                                                                     P]
+        L.ltd_tree_accept_sampling.restype = i32
         L.ltd_version.argtypes = []
         L.ltd_version.restype = ctypes.c_char_p
         _lib = L
@@ -268,3 +275,23 @@ def draft_expand(logits, frontier, scores, pool_parents, pool_tokens, pool_size,
         _p(pool_parents), _p(pool_tokens), _p(pool_size), Vpool, _p(new_frontier), _p(workspace),
         workspace.numel() * workspace.element_size(), int(validate), _p(status), _stream(stream))
     _check("ltd_draft_expand", rc)
+
+
+def accept_sampling_workspace_size(B, Nmax, Voc) -> int:
+    return int(lib().ltd_tree_accept_sampling_workspace_size(B, Nmax, Voc))
+
+
+def tree_accept_sampling(logits, draft_probs, draft_tokens, parents, n_nodes, uniforms,
+                         accepted_nodes, out_tokens, n_accepted, *, temperature: float = 1.0,
+                         workspace=None, validate: bool = False, status=None, stream=None):
+    """Acceptance by recursive rejection sampling at temperature T > 0; see
+    ``ltd_tree_accept_sampling``."""
+    B, Nmax, Voc = logits.shape
+    if workspace is None:
+        workspace = _alloc_workspace(accept_sampling_workspace_size(B, Nmax, Voc), logits.device)
+    rc = lib().ltd_tree_accept_sampling(
+        _p(logits), _p(draft_probs), _p(draft_tokens), _p(parents), _p(n_nodes), _p(uniforms), B,
+        Nmax, Voc, float(temperature), _p(accepted_nodes), _p(out_tokens), _p(n_accepted),
+        _p(workspace), workspace.numel() * workspace.element_size(), int(validate), _p(status),
+        _stream(stream))
+    _check("ltd_tree_accept_sampling", rc)

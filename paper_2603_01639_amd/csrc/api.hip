@@ -187,6 +187,43 @@ int ltd_select_candidates(const float* scores, const int32_t* pool_parents,
   return LTD_OK;
 }
 
+size_t ltd_tree_accept_sampling_workspace_size(int B, int Nmax, int Voc) {
+  if (B < 0 || Nmax < 1 || Nmax > LTD_MAX_NODES || Voc < 1 ||
+      ltd::sampling_chunks(Voc) > LTD_SAMPLING_MAX_CHUNKS)
+    return 0;
+  return ltd::sampling_workspace_bytes(B, Nmax, Voc);
+}
+
+int ltd_tree_accept_sampling(const float* logits, const float* draft_probs,
+                             const int32_t* draft_tokens, const int32_t* parents,
+                             const int32_t* n_nodes, const float* uniforms, int B, int Nmax,
+                             int Voc, float temperature, int32_t* accepted_nodes,
+                             int32_t* out_tokens, int32_t* n_accepted, void* workspace,
+                             size_t workspace_bytes, int validate, int32_t* status, void* stream) {
+  if (B < 0 || Nmax < 1 || Nmax > LTD_MAX_NODES || Voc < 1 ||
+      ltd::sampling_chunks(Voc) > LTD_SAMPLING_MAX_CHUNKS || !(temperature > 0.f) ||
+      !std::isfinite(temperature))
+    return LTD_EINVAL;
+  if (validate && !status) return LTD_EINVAL;
+  if (B == 0) return LTD_OK;
+  if (!logits || !draft_probs || !draft_tokens || !parents || !n_nodes || !uniforms ||
+      !accepted_nodes || !out_tokens || !n_accepted)
+    return LTD_EINVAL;
+  if (!workspace || workspace_bytes < ltd::sampling_workspace_bytes(B, Nmax, Voc))
+    return LTD_EWORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (validate) {
+    if (ltd::launch_validate_tree(nullptr, nullptr, parents, n_nodes, B, Nmax, 0, 1, 0, 0, false,
+                                  status, st) != hipSuccess)
+      return LTD_EHIP;
+  }
+  if (ltd::launch_sampling(logits, draft_probs, draft_tokens, parents, n_nodes, uniforms, B, Nmax,
+                           Voc, temperature, accepted_nodes, out_tokens, n_accepted, workspace,
+                           validate ? status : nullptr, st) != hipSuccess)
+    return LTD_EHIP;
+  return LTD_OK;
+}
+
 namespace {
 bool expand_args_ok(int B, int F, int Voc, int W) {
   return B >= 0 && F >= 1 && W >= 1 && W <= LTD_EXPAND_MAX_W && Voc >= W &&

@@ -66,6 +66,16 @@ hipError_t launch_select(const float* scores, const int32_t* pool_parents,
                          int32_t* parents, int32_t* tokens, int32_t* depth, int32_t* n_nodes,
                          const int32_t* status, hipStream_t stream);
 
+// sample.hip
+int sampling_chunks(int Voc);
+size_t sampling_workspace_bytes(int B, int Nmax, int Voc);
+hipError_t launch_sampling(const float* logits, const float* draft_probs,
+                           const int32_t* draft_tokens, const int32_t* parents,
+                           const int32_t* n_nodes, const float* uniforms, int B, int Nmax,
+                           int Voc, float temperature, int32_t* accepted_nodes,
+                           int32_t* out_tokens, int32_t* n_accepted, void* workspace,
+                           const int32_t* status, hipStream_t stream);
+
 // expand.hip
 int expand_chunks(int Voc);
 size_t expand_workspace_bytes(int B, int F, int Voc, int W);

@@ -530,3 +530,72 @@ def policy_batch(layout: int, B: int, rep: int = 0) -> PolicyBatch:
     return PolicyBatch(layout, dims, layers, sb.scores, sb.pool_size, np.array(depths, np.int32),
                        ctx, off, scale, label=f"{name} policy B{B} dims {dims}",
                        pool_parents=sb.pool_parents, pool_tokens=sb.pool_tokens)
+
+
+# ------------------------------------------------------ sampling acceptance
+
+@dataclasses.dataclass
+class SamplingBatch:
+    """Inputs of acceptance at temperature T: the target logits at every
+    node, the draft distribution at every node with children (zeros
+    elsewhere), child tokens drawn from it without replacement in ascending
+    node order, and the uniforms of every decision."""
+    logits: np.ndarray  # float32 [B][Nmax][Voc]
+    draft_probs: np.ndarray  # float32 [B][Nmax][Voc]
+    draft_tokens: np.ndarray  # int32 [B][Nmax]
+    parents: np.ndarray  # int32 [B][Nmax]
+    n_nodes: np.ndarray  # int32 [B]
+    uniforms: np.ndarray  # float32 [B][Nmax][2] in [0, 1)
+    temperature: float
+    label: str = ""
+
+    @property
+    def B(self) -> int:
+        return self.logits.shape[0]
+
+
+def _softmax_rows(x: np.ndarray) -> np.ndarray:
+    e = np.exp(x - x.max(axis=-1, keepdims=True))
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def make_sampling_batch(rng: np.random.Generator, trees: List[np.ndarray], Voc: int, *,
+                        temperature: float = 1.0, logit_scale: float = 3.0,
+                        draft_noise: float = 1.0, Nmax: Optional[int] = None,
+                        label: str = "") -> SamplingBatch:
+    """Target logits N(0, logit_scale^2); the draft distribution at a node is
+    softmax((logits + N(0, draft_noise^2)) / T) (draft_noise = 0: the draft
+    equals the target); a node's children take tokens drawn without
+    replacement from it (Gumbel top-k), in ascending node order."""
+    B = len(trees)
+    Nmax = Nmax or max(len(t) for t in trees)
+    logits = (rng.standard_normal((B, Nmax, Voc)) * logit_scale).astype(np.float32)
+    q = np.zeros((B, Nmax, Voc), np.float32)
+    toks = np.zeros((B, Nmax), np.int32)
+    par = np.full((B, Nmax), -1, np.int32)
+    for b, tr in enumerate(trees):
+        n = len(tr)
+        par[b, :n] = tr
+        for u in range(n):
+            kids = [c for c in range(u + 1, n) if tr[c] == u]
+            if not kids:
+                continue
+            noisy = logits[b, u].astype(np.float64)
+            if draft_noise > 0:
+                noisy = noisy + rng.standard_normal(Voc) * draft_noise
+            qu = _softmax_rows(noisy / temperature)
+            q[b, u] = qu.astype(np.float32)
+            g = np.log(np.maximum(qu, 1e-300)) - np.log(-np.log(rng.random(Voc)))
+            order = np.argsort(-g, kind="stable")[:len(kids)]
+            toks[b, kids] = order.astype(np.int32)
+    uni = np.minimum(rng.random((B, Nmax, 2)), 1.0 - 2.0 ** -24).astype(np.float32)
+    return SamplingBatch(logits, q, toks, par, np.array([len(t) for t in trees], np.int32), uni,
+                         float(temperature), label)
+
+
+def sampling_8b(rep: int = 0) -> SamplingBatch:
+    """The 8B-shaped step at T = 1: one 60-node Eagle tree (depth 6, top-10)
+    over a 128256-token vocabulary."""
+    rng = rng_for(config_seed(12, rep))
+    t = tree_eagle(rng, 60, 6, 10, 128256)
+    return make_sampling_batch(rng, [t.parents], 128256, label="sampling 8B T=1 N60")

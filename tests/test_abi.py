@@ -157,3 +157,19 @@ def test_draft_expand_rejects_bad_scalar_arguments(B, F, Voc, W, W_next):
 def test_draft_expand_workspace():
     assert ltd.draft_expand_workspace_size(2, 10, 128256, 10) == 2 * 10 * 32 * (8 * 10 + 8)
     assert ltd.draft_expand_workspace_size(1, 1, 64 * 4096 + 1, 4) == 0
+
+
+@pytest.mark.parametrize("args", [dict(B=-1), dict(Nmax=0), dict(Nmax=257), dict(Voc=0),
+                                  dict(Voc=64 * 4096 + 1), dict(T=0.0), dict(T=-1.0),
+                                  dict(T=float("inf")), dict(T=float("nan"))])
+def test_sampling_rejects_bad_scalar_arguments(args):
+    P = 0x1000
+    a = dict(B=1, Nmax=60, Voc=128256, T=1.0)
+    a.update(args)
+    rc = ltd.lib().ltd_tree_accept_sampling(P, P, P, P, P, P, a["B"], a["Nmax"], a["Voc"], a["T"],
+                                            P, P, P, P, 1 << 30, 0, None, None)
+    assert rc == ltd.LTD_EINVAL
+
+
+def test_sampling_workspace():
+    assert ltd.accept_sampling_workspace_size(1, 60, 128256) == 60 * 32 * 16
