@@ -123,18 +123,24 @@ __global__ void __launch_bounds__(kStatThreads) sample_stats_kernel(
   }
 }
 
-// One thread's share of sum_v max(P(v) - g Q(v), 0) with P(v) = exp(l_v/T -
-// M) / Z and Q(v) = q_v / QS: float4 loads of both rows in batches of
-// kBatch, all issued before any use (a strided, coalesced layout; rows of a
-// vocabulary that is not a multiple of 4 take the scalar tail path).
-constexpr int kBatch = 4;
-__device__ __forceinline__ float residual_elem(float l, float q, float inv_t, float Mf,
-                                               float inv_zf, float inv_qsf, float g) {
-  const float p = __expf(l * inv_t - Mf) * inv_zf;
-  return fmaxf(p - g * (q * inv_qsf), 0.f);
+// The residual R(v) = max(P(v) - g Q(v), 0) of one node, with P(v) =
+// exp(l_v/T - M) / Z and Q(v) = q_v / QS, as one FMA, one exp2 and one FMA
+// per token: P(v) = 2^(l_v a - b) with a = log2(e)/T and b = log2(e) (M +
+// ln Z), and g Q(v) = gq q_v with gq = g / QS.
+struct Residual {
+  float a, b, gq;
+};
+__device__ __forceinline__ float residual_elem(float l, float q, const Residual& r) {
+  const float p = __builtin_amdgcn_exp2f(fmaf(l, r.a, -r.b));
+  return fmaxf(fmaf(-r.gq, q, p), 0.f);
 }
+
+// One thread's share of sum_v R(v): float4 loads of both rows in batches of
+// kBatch, all issued before any use (a strided, coalesced layout; rows of a
+// vocabulary that is not a multiple of 4 take the scalar path).
+constexpr int kBatch = 4;
 __device__ float residual_pass(const float* __restrict__ l, const float* __restrict__ q, int Voc,
-                               int t, float inv_t, float Mf, float inv_zf, float inv_qsf, float g) {
+                               int t, const Residual& r) {
   float part = 0.f;
   const bool aligned = (Voc & 3) == 0 && (reinterpret_cast<uintptr_t>(l) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(q) & 15) == 0;
@@ -153,10 +159,10 @@ __device__ float residual_pass(const float* __restrict__ l, const float* __restr
 #pragma unroll
       for (int k = 0; k < kBatch; ++k) {
         if (i0 + k * kWalkThreads < n4) {
-          part += residual_elem(lv[k].x, qv[k].x, inv_t, Mf, inv_zf, inv_qsf, g);
-          part += residual_elem(lv[k].y, qv[k].y, inv_t, Mf, inv_zf, inv_qsf, g);
-          part += residual_elem(lv[k].z, qv[k].z, inv_t, Mf, inv_zf, inv_qsf, g);
-          part += residual_elem(lv[k].w, qv[k].w, inv_t, Mf, inv_zf, inv_qsf, g);
+          part += residual_elem(lv[k].x, qv[k].x, r);
+          part += residual_elem(lv[k].y, qv[k].y, r);
+          part += residual_elem(lv[k].z, qv[k].z, r);
+          part += residual_elem(lv[k].w, qv[k].w, r);
         }
       }
     }
@@ -172,7 +178,7 @@ __device__ float residual_pass(const float* __restrict__ l, const float* __restr
 #pragma unroll
       for (int k = 0; k < kBatch; ++k)
         if (v0 + k * kWalkThreads < Voc)
-          part += residual_elem(lv[k], qv[k], inv_t, Mf, inv_zf, inv_qsf, g);
+          part += residual_elem(lv[k], qv[k], r);
     }
   }
   return part;
@@ -214,8 +220,7 @@ __device__ double block_sum(double v, double* red_s, int lane, int w) {
 // multiples of 4 and the rows 16-byte aligned), kBatch loads in flight.
 template <bool kVec>
 __device__ double wave_range_sum(const float* __restrict__ l, const float* __restrict__ q, int lo,
-                                 int hi, int lane, bool use_q, float inv_t, float Mf, float inv_zf,
-                                 float inv_qsf, float g) {
+                                 int hi, int lane, bool use_q, const Residual& r) {
   double acc = 0.0;
   if (kVec) {
     constexpr int kStep = 4 * kWave;
@@ -230,11 +235,11 @@ __device__ double wave_range_sum(const float* __restrict__ l, const float* __res
 #pragma unroll
       for (int k = 0; k < kBatch; ++k) {
         if (v0 + k * kStep < hi) {
-          float r = residual_elem(lv[k].x, qv[k].x, inv_t, Mf, inv_zf, inv_qsf, g);
-          r += residual_elem(lv[k].y, qv[k].y, inv_t, Mf, inv_zf, inv_qsf, g);
-          r += residual_elem(lv[k].z, qv[k].z, inv_t, Mf, inv_zf, inv_qsf, g);
-          r += residual_elem(lv[k].w, qv[k].w, inv_t, Mf, inv_zf, inv_qsf, g);
-          acc += static_cast<double>(r);
+          float sum4 = residual_elem(lv[k].x, qv[k].x, r);
+          sum4 += residual_elem(lv[k].y, qv[k].y, r);
+          sum4 += residual_elem(lv[k].z, qv[k].z, r);
+          sum4 += residual_elem(lv[k].w, qv[k].w, r);
+          acc += static_cast<double>(sum4);
         }
       }
     }
@@ -250,7 +255,7 @@ __device__ double wave_range_sum(const float* __restrict__ l, const float* __res
 #pragma unroll
       for (int k = 0; k < kBatch; ++k)
         if (v0 + k * kWave < hi)
-          acc += static_cast<double>(residual_elem(lv[k], qv[k], inv_t, Mf, inv_zf, inv_qsf, g));
+          acc += static_cast<double>(residual_elem(lv[k], qv[k], r));
     }
   }
   return wave_sum_d(acc, lane);
@@ -334,8 +339,11 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
     const float Mf = static_cast<float>(node_s[0]);
     const double Z = node_s[1];
     const double QS = node_s[2];
-    const float inv_zf = static_cast<float>(1.0 / Z);
-    const float inv_qsf = QS > 0.0 ? static_cast<float>(1.0 / QS) : 0.f;
+    constexpr double kLog2e = 1.4426950408889634;
+    Residual res;
+    res.a = static_cast<float>(kLog2e * static_cast<double>(inv_t));
+    res.b = static_cast<float>(kLog2e * (static_cast<double>(Mf) + log(Z)));
+    res.gq = 0.f;
 
     double g = 0.0, s = 1.0, D = 0.0;  // the residual after the rejections so far
     int n_removed = 0;
@@ -360,9 +368,8 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
         }
         // rejected: the next residual needs one pass over the vocabulary
         const double g2 = g + s / (1.0 - D);
-        const float g2f = static_cast<float>(g2);
-        const float part = residual_pass(logits + row, draft_probs + row, Voc, t, inv_t, Mf,
-                                         inv_zf, inv_qsf, g2f);
+        res.gq = QS > 0.0 ? static_cast<float>(g2 / QS) : 0.f;
+        const float part = residual_pass(logits + row, draft_probs + row, Voc, t, res);
         const double s2 = block_sum(static_cast<double>(part), red_s, lane, w);
         if (t == 0) removed_s[n_removed] = x;
         __syncthreads();
@@ -389,8 +396,8 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
     // fewer wave 0 takes an inclusive scan and the first token past the
     // target.  Where rounding leaves the target at or past a level's sum, the
     // last segment (token) with mass is taken, as the plain scan would.
-    const float gf = static_cast<float>(g);
     const bool use_q = g > 0.0;
+    res.gq = use_q && QS > 0.0 ? static_cast<float>(g / QS) : 0.f;
     const bool vec = (Voc & 3) == 0 && (reinterpret_cast<uintptr_t>(logits + row) & 15) == 0 &&
                      (reinterpret_cast<uintptr_t>(draft_probs + row) & 15) == 0;
     int lo = 0, hi = Voc;
@@ -401,10 +408,8 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
                           : (span + kWalkWaves - 1) / kWalkWaves;
       const int s_lo = min(lo + w * seg, hi), s_hi = min(s_lo + seg, hi);
       const double sum =
-          vec ? wave_range_sum<true>(logits + row, draft_probs + row, s_lo, s_hi, lane, use_q,
-                                     inv_t, Mf, inv_zf, inv_qsf, gf)
-              : wave_range_sum<false>(logits + row, draft_probs + row, s_lo, s_hi, lane, use_q,
-                                      inv_t, Mf, inv_zf, inv_qsf, gf);
+          vec ? wave_range_sum<true>(logits + row, draft_probs + row, s_lo, s_hi, lane, use_q, res)
+              : wave_range_sum<false>(logits + row, draft_probs + row, s_lo, s_hi, lane, use_q, res);
       if (lane == 0) red_s[w] = sum;
       __syncthreads();
       if (t == 0) {
@@ -445,7 +450,7 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
       float rv = 0.f;
       if (v < hi) {
         const float qv = use_q ? draft_probs[row + v] : 0.f;
-        rv = residual_elem(logits[row + v], qv, inv_t, Mf, inv_zf, inv_qsf, gf);
+        rv = residual_elem(logits[row + v], qv, res);
       }
       double incl = static_cast<double>(rv);
 #pragma unroll
