@@ -82,15 +82,16 @@ def test_replays_the_generators_beam_on_the_gpu():
 
 @pytest.mark.parametrize("B,F,Voc,Wd,W_next", [
     (1, 1, 128256, 10, 10), (1, 10, 128256, 10, 10), (4, 10, 152064, 10, 10), (2, 3, 4097, 4, 7),
-    (3, 16, 262144, 16, 16), (2, 1, 16, 16, 5), (1, 5, 10, 1, 3), (2, 7, 4095, 3, 21)])
+    (3, 16, 262144, 16, 16), (2, 1, 16, 16, 5), (1, 5, 10, 1, 3), (2, 7, 4095, 3, 21),
+    (2, 40, 5000, 4, 12), (1, 256, 100, 1, 64)])
 def test_random_logits(B, F, Voc, Wd, W_next):
     rng = np.random.default_rng(Voc + F * 100 + Wd)
     logits = (rng.standard_normal((B, F, Voc)) * 2).astype(np.float32)
-    Vpool = 30 + F * Wd + 5
+    Vpool = max(30, F + 1) + F * Wd + 5
     scores = (-rng.random((B, Vpool)) * 10).astype(np.float32)
     par = rng.integers(-1, 5, size=(B, Vpool)).astype(np.int32)
     tok = rng.integers(0, 100, size=(B, Vpool)).astype(np.int32)
-    size = rng.integers(F, 31, size=B).astype(np.int32)
+    size = rng.integers(F, max(31, F + 2), size=B).astype(np.int32)
     frontier = np.stack([rng.choice(size[b], F, replace=False) for b in range(B)]).astype(np.int32)
     U.log(f"[expand] random B={B} F={F} Voc={Voc} W={Wd} W_next={W_next}")
     pool = (scores, par, tok, size)
@@ -114,6 +115,32 @@ def test_tied_logits():
     want = oracle.draft_expand(logits, frontier, *pool, W=10, W_next=10)
     _compare(got, want, pool[3], "ties")
     assert got[2][0, 5:15].tolist() == list(range(10))
+
+
+def test_crowded_thresholds():
+    """Rows built so that many keys pass the selection thresholds: in node 0,
+    ten runs of four consecutive tokens in every 1024-token block of the first
+    4096-token chunk carry large, nearly equal values (so whole runs sit just
+    above the chunk's threshold); in node 1 the ten largest values of each of
+    the first ten chunks are all larger than the tenth-largest chunk maximum.
+    Both are exact against the oracle."""
+    rng = np.random.default_rng(17)
+    B, F, Voc, W = 1, 2, 50000, 10
+    logits = rng.standard_normal((B, F, Voc)).astype(np.float32)
+    for t in range(10):
+        for j in range(4):
+            for e in range(4):
+                logits[0, 0, j * 1024 + t * 4 + e] = 100 + t * 0.01 + (j * 4 + e) * 1e-4
+    for c in range(10):
+        pos = c * 4096 + rng.choice(4096, 10, replace=False)
+        logits[0, 1, pos] = 50 + c * 0.01 + np.arange(10) * 1e-4
+    pool = TE._empty_pool(B, 64)
+    pool[3][:] = 5
+    frontier = np.array([[0, 3]], np.int32)
+    U.log("[expand] crowded thresholds")
+    got = _gpu_round(logits, frontier, pool, W, W)
+    want = oracle.draft_expand(logits, frontier, *pool, W=W, W_next=W)
+    _compare(got, want, pool[3], "crowded")
 
 
 def test_validation():
