@@ -170,9 +170,22 @@ def main():
 
     # A plain device copy of known size, outside the timed region: under
     # rocprofv3 counter collection it calibrates FETCH_SIZE / WRITE_SIZE.
+    # Timed repeats of the same copy give the box's measured copy bandwidth
+    # (read + write bytes over time), the practical ceiling beside the 8 TB/s
+    # datasheet peak.
     calib = torch.empty(CALIB_BYTES, dtype=torch.uint8, device="cuda")
     calib2 = torch.empty_like(calib)
     calib2.copy_(calib)
+    torch.cuda.synchronize()
+    c0 = torch.cuda.Event(enable_timing=True)
+    c1 = torch.cuda.Event(enable_timing=True)
+    n_copy = 5
+    c0.record()
+    for _ in range(n_copy):
+        calib2.copy_(calib)
+    c1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 2 * CALIB_BYTES * n_copy / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del calib, calib2
 
     for i in range(args.warmup):
@@ -342,8 +355,21 @@ def main():
                          "GB/s": round(wbytes / (p_us * 1e-6) / 1e9, 1), "in_value": False}
     dom = max(("tree_verify_attn", "tree_accept"), key=lambda n: per_call_us[n])
     traffic = read_traffic(args.traffic, args.workload, dom)
-    roof = {"kernel": dom, "bound": "hbm", "achieved": kernels[dom]["GB/s"], "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": kernels[dom]["hbm_frac"], "traffic": traffic}
+    # The binding roof of the dominant call: attention is MFMA-bound once its
+    # FLOPs take longer at the bf16 peak than its bytes at the HBM peak.
+    dom_flops = flops if dom == "tree_verify_attn" else 0
+    t_hbm = kernels[dom]["alg_bytes"] / (HBM_PEAK_GBS * 1e9)
+    t_mfma = dom_flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+    if t_mfma > t_hbm:
+        roof = {"kernel": dom, "bound": "mfma", "achieved": kernels[dom]["TFLOP/s"],
+                "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(t_mfma / (per_call_us[dom] * 1e-6), 4)}
+    else:
+        roof = {"kernel": dom, "bound": "hbm", "achieved": kernels[dom]["GB/s"],
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kernels[dom]["hbm_frac"]}
+    roof.update({"traffic": traffic, "hbm_GBps": kernels[dom]["GB/s"],
+                 "copy_GBps": round(copy_gbs, 1),
+                 "hbm_frac_of_copy": round(kernels[dom]["GB/s"] / copy_gbs, 4)})
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -408,8 +434,8 @@ def cpu_baseline(b, seconds):
     """The CPU oracle (fp64 C, OpenMP) on whole verify steps of the same
     workload, repeated for about `seconds` of wall time."""
     import oracle
-    reps, t_start = 0, time.perf_counter()
-    while True:
+
+    def one_step():
         oracle.tree_verify_attn(b.q, b.k_cache, b.v_cache, b.prefix_len, b.parents, b.n_nodes,
                                 Hkv=b.Hkv, block_table=b.block_table, num_blocks=b.num_blocks,
                                 dtype=b.dtype)
@@ -417,14 +443,39 @@ def cpu_baseline(b, seconds):
         k, v = b.k_cache.copy(), b.v_cache.copy()
         oracle.kv_compact(k, v, b.prefix_len, acc, nacc, Hkv=b.Hkv, block_table=b.block_table,
                           num_blocks=b.num_blocks)
+
+    reps, t_start = 0, time.perf_counter()
+    while True:
+        one_step()
         reps += 1
         el = time.perf_counter() - t_start
         if el >= seconds or reps >= 1000:
             break
-    return {"value": round(el / reps * 1e6, 1), "unit": "µs", "cores": oracle.num_threads(),
+    cores = oracle.num_threads()
+    # the same step on one core, a few repetitions
+    oracle.set_num_threads(1)
+    one_reps, t1 = 0, time.perf_counter()
+    while True:
+        one_step()
+        one_reps += 1
+        el1 = time.perf_counter() - t1
+        if el1 >= min(seconds, 6.0) or one_reps >= 1000:
+            break
+    oracle.set_num_threads(cores)
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": round(el / reps * 1e6, 1), "unit": "µs", "cores": cores,
             "kind": "oracle",
             "sample": f"{reps} whole verify steps of the benchmark workload (attention for every "
-                      f"node and head, acceptance, compaction incl. a cache copy), fp64 C oracle"}
+                      f"node and head, acceptance, compaction incl. a cache copy), fp64 C oracle",
+            "one_core_value": round(el1 / one_reps * 1e6, 1), "one_core_steps": one_reps,
+            "cpu_model": model}
 
 
 if __name__ == "__main__":

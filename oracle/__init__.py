@@ -62,6 +62,8 @@ def load_library(path: str) -> ctypes.CDLL:
     lib.ltd_oracle_tree_accept_sampling.restype = i32
     lib.ltd_oracle_num_threads.argtypes = []
     lib.ltd_oracle_num_threads.restype = i32
+    lib.ltd_oracle_set_num_threads.argtypes = [i32]
+    lib.ltd_oracle_set_num_threads.restype = None
     return lib
 
 
@@ -85,6 +87,11 @@ def _c(a, dtype):
 
 def num_threads() -> int:
     return int(_load().ltd_oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads for the oracle's OpenMP loops from now on (timing only)."""
+    _load().ltd_oracle_set_num_threads(int(n))
 
 
 def tree_verify_attn(q, k_cache, v_cache, prefix_len, parents, n_nodes, *, Hkv, block_table=None,

@@ -56,6 +56,15 @@ int ltd_oracle_num_threads(void) {
 #endif
 }
 
+/* Threads for the next parallel regions (n >= 1); no effect without OpenMP. */
+void ltd_oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* bf16 is the top half of an IEEE binary32; widening is exact. */
 static double bf16_bits_to_double(uint16_t bits) {
   uint32_t u = (uint32_t)bits << 16;

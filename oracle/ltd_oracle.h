@@ -116,6 +116,9 @@ int ltd_oracle_draft_expand(const float* logits, const int32_t* frontier, int B,
 
 /* Threads the oracle's parallel loops use (OpenMP), for reporting. */
 int ltd_oracle_num_threads(void);
+/* Threads for the next parallel regions (n >= 1; timing only: results do not
+ * depend on it). */
+void ltd_oracle_set_num_threads(int n);
 
 #ifdef __cplusplus
 }
