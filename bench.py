@@ -355,18 +355,8 @@ def main():
                          "GB/s": round(wbytes / (p_us * 1e-6) / 1e9, 1), "in_value": False}
     dom = max(("tree_verify_attn", "tree_accept"), key=lambda n: per_call_us[n])
     traffic = read_traffic(args.traffic, args.workload, dom)
-    # The binding roof of the dominant call: attention is MFMA-bound once its
-    # FLOPs take longer at the bf16 peak than its bytes at the HBM peak.
-    dom_flops = flops if dom == "tree_verify_attn" else 0
-    t_hbm = kernels[dom]["alg_bytes"] / (HBM_PEAK_GBS * 1e9)
-    t_mfma = dom_flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
-    if t_mfma > t_hbm:
-        roof = {"kernel": dom, "bound": "mfma", "achieved": kernels[dom]["TFLOP/s"],
-                "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(t_mfma / (per_call_us[dom] * 1e-6), 4)}
-    else:
-        roof = {"kernel": dom, "bound": "hbm", "achieved": kernels[dom]["GB/s"],
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kernels[dom]["hbm_frac"]}
+    roof = binding_roof(dom, kernels[dom]["alg_bytes"],
+                        flops if dom == "tree_verify_attn" else 0, per_call_us[dom])
     roof.update({"traffic": traffic, "hbm_GBps": kernels[dom]["GB/s"],
                  "copy_GBps": round(copy_gbs, 1),
                  "hbm_frac_of_copy": round(kernels[dom]["GB/s"] / copy_gbs, 4)})
@@ -398,6 +388,20 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
+
+
+def binding_roof(call, alg_bytes, alg_flops, us):
+    """The roof that binds a call: MFMA (bf16 dense peak) when its FLOPs take
+    longer there than its algorithmic bytes at the HBM peak, else HBM.  frac =
+    that ideal time / the measured time."""
+    t_hbm = alg_bytes / (HBM_PEAK_GBS * 1e9)
+    t_mfma = alg_flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+    t = us * 1e-6
+    if t_mfma > t_hbm:
+        return {"kernel": call, "bound": "mfma", "achieved": round(alg_flops / t / 1e12, 2),
+                "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(t_mfma / t, 4)}
+    return {"kernel": call, "bound": "hbm", "achieved": round(alg_bytes / t / 1e9, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(t_hbm / t, 4)}
 
 
 # The kernel sources behind each call's counters (launch plan included).
