@@ -323,7 +323,8 @@ def main():
     kernels["tree_accept_sampling"] = {
         "us": round(s_us, 3), "workload": smp.label, "n_accepted": s_nacc,
         "note": "T = 1; the draft distributions and uniforms are inputs; cost grows with the "
-                "rejections on the accepted path (one vocabulary pass each)",
+                "rejections on the accepted path (one vocabulary pass each after a "
+                "node's first)",
         "in_value": False}
 
     # ---- draft policies, outside the step (graphs of K calls), one state

@@ -184,6 +184,55 @@ __device__ float residual_pass(const float* __restrict__ l, const float* __restr
   return part;
 }
 
+// The node's softmax maximum (float, logits / T units), normaliser Z and
+// draft-row sum QS (double) from its chunk partials, by one wave (lane c
+// takes chunk c), in the same order wherever it is called, so every kernel
+// derives bit-identical residual parameters.
+struct NodeTotals {
+  float Mf;
+  double Z, QS;
+};
+__device__ NodeTotals merge_node_stats(const NodeStats* __restrict__ st_row, int chunks, int lane) {
+  const NodeStats st = st_row[min(lane, chunks - 1)];
+  const float m_l = lane < chunks ? st.m : -INFINITY;
+  float Mf = m_l;
+  Mf = fmaxf(Mf, lane_xor_f<32>(Mf, lane));
+  Mf = fmaxf(Mf, lane_xor_f<16>(Mf, lane));
+  Mf = fmaxf(Mf, lane_xor_f<8>(Mf, lane));
+  Mf = fmaxf(Mf, lane_xor_f<4>(Mf, lane));
+  Mf = fmaxf(Mf, lane_xor_f<2>(Mf, lane));
+  Mf = fmaxf(Mf, lane_xor_f<1>(Mf, lane));
+  double zl =
+      m_l != -INFINITY ? static_cast<double>(st.z) * exp(static_cast<double>(m_l - Mf)) : 0.0;
+  double ql = lane < chunks ? static_cast<double>(st.qs) : 0.0;
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) {
+    uint64_t oz, oq;
+    const uint64_t bz = static_cast<uint64_t>(__double_as_longlong(zl));
+    const uint64_t bq = static_cast<uint64_t>(__double_as_longlong(ql));
+    switch (d) {
+      case 32: oz = lane_xor_u64<32>(bz, lane); oq = lane_xor_u64<32>(bq, lane); break;
+      case 16: oz = lane_xor_u64<16>(bz, lane); oq = lane_xor_u64<16>(bq, lane); break;
+      case 8: oz = lane_xor_u64<8>(bz, lane); oq = lane_xor_u64<8>(bq, lane); break;
+      case 4: oz = lane_xor_u64<4>(bz, lane); oq = lane_xor_u64<4>(bq, lane); break;
+      case 2: oz = lane_xor_u64<2>(bz, lane); oq = lane_xor_u64<2>(bq, lane); break;
+      default: oz = lane_xor_u64<1>(bz, lane); oq = lane_xor_u64<1>(bq, lane);
+    }
+    zl += __longlong_as_double(static_cast<long long>(oz));
+    ql += __longlong_as_double(static_cast<long long>(oq));
+  }
+  return NodeTotals{Mf, zl, ql};
+}
+
+constexpr double kLog2e = 1.4426950408889634;
+__device__ __forceinline__ Residual residual_params(const NodeTotals& nt, float inv_t, double g) {
+  Residual r;
+  r.a = static_cast<float>(kLog2e * static_cast<double>(inv_t));
+  r.b = static_cast<float>(kLog2e * (static_cast<double>(nt.Mf) + log(nt.Z)));
+  r.gq = g > 0.0 && nt.QS > 0.0 ? static_cast<float>(g / nt.QS) : 0.f;
+  return r;
+}
+
 // Wave-wide double sum (every lane gets it).
 __device__ __forceinline__ double wave_sum_d(double v, int lane) {
 #pragma unroll
@@ -261,19 +310,88 @@ __device__ double wave_range_sum(const float* __restrict__ l, const float* __res
   return wave_sum_d(acc, lane);
 }
 
+// Per (node, chunk): the residual mass sum_v max(P(v) - g Q(v), 0) over the
+// chunk at g = 0 (the softmax mass) and, for nodes with children, at g = 1
+// (after the node's first rejection, g is exactly 1), with the walk's own
+// parameters and element arithmetic.
+__global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
+    const float* __restrict__ logits, const float* __restrict__ draft_probs,
+    const int32_t* __restrict__ parents, const int32_t* __restrict__ n_nodes, int Nmax, int Voc,
+    float inv_t, const NodeStats* __restrict__ ws, double2* __restrict__ mass,
+    const int32_t* status) {
+  __shared__ NodeTotals nt_s;
+  __shared__ int has_child_s;
+  __shared__ double red_s[2][kStatThreads / kWave];
+  if (halted(status)) return;
+  const int chunk = blockIdx.x, i = blockIdx.y, b = blockIdx.z;
+  const int chunks = gridDim.x;
+  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  const int n = min(max(n_nodes[b], 1), Nmax);
+  if (i >= n) return;  // uniform for the block
+  const int64_t nb = static_cast<int64_t>(b) * Nmax;
+  const int64_t row = (nb + i) * Voc;
+  const int base = chunk * kChunk;
+  float l[kPerThread];
+#pragma unroll
+  for (int k = 0; k < kPerThread; ++k) l[k] = logits[row + min(base + k * kStatThreads + t, Voc - 1)];
+  if (t == 0) has_child_s = 0;
+  if (w == 0) {
+    const NodeTotals nt = merge_node_stats(ws + (nb + i) * chunks, chunks, lane);
+    if (lane == 0) nt_s = nt;
+  }
+  __syncthreads();
+  for (int j = t; j < n; j += kStatThreads)
+    if (parents[nb + j] == i && j > i) has_child_s = 1;
+  __syncthreads();
+  const bool want_q = has_child_s != 0;
+  float q[kPerThread];
+#pragma unroll
+  for (int k = 0; k < kPerThread; ++k)
+    q[k] = want_q ? draft_probs[row + min(base + k * kStatThreads + t, Voc - 1)] : 0.f;
+  const NodeTotals nt = nt_s;
+  const Residual r0 = residual_params(nt, inv_t, 0.0);
+  const Residual r1 = residual_params(nt, inv_t, 1.0);
+  double d0 = 0.0, d1 = 0.0;
+#pragma unroll
+  for (int k = 0; k < kPerThread; ++k) {
+    if (base + k * kStatThreads + t < Voc) {
+      d0 += static_cast<double>(residual_elem(l[k], 0.f, r0));
+      d1 += static_cast<double>(residual_elem(l[k], q[k], r1));
+    }
+  }
+  d0 = wave_sum_d(d0, lane);
+  d1 = wave_sum_d(d1, lane);
+  if (lane == 0) {
+    red_s[0][w] = d0;
+    red_s[1][w] = d1;
+  }
+  __syncthreads();
+  if (t == 0) {
+    double a0 = 0.0, a1 = 0.0;
+#pragma unroll
+    for (int k = 0; k < kStatThreads / kWave; ++k) {
+      a0 += red_s[0][k];
+      a1 += red_s[1][k];
+    }
+    mass[(nb + i) * chunks + chunk] = make_double2(a0, want_q ? a1 : 0.0);
+  }
+}
+
 __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
     const float* __restrict__ logits, const float* __restrict__ draft_probs,
     const int32_t* __restrict__ draft_tokens, const int32_t* __restrict__ parents,
     const int32_t* __restrict__ n_nodes, const float* __restrict__ uniforms, int Nmax, int Voc,
-    float inv_t, const NodeStats* __restrict__ ws, int chunks, int32_t* __restrict__ accepted,
-    int32_t* __restrict__ out_tokens, int32_t* __restrict__ n_accepted, const int32_t* status) {
+    float inv_t, const NodeStats* __restrict__ ws, const double2* __restrict__ mass, int chunks,
+    int32_t* __restrict__ accepted, int32_t* __restrict__ out_tokens,
+    int32_t* __restrict__ n_accepted, const int32_t* status) {
   __shared__ int32_t par_s[LTD_MAX_NODES];
   __shared__ int32_t tok_s[LTD_MAX_NODES];
   __shared__ uint64_t child_s[LTD_MAX_NODES / kWave];
   __shared__ int32_t path_s[LTD_MAX_NODES];
   __shared__ int32_t removed_s[LTD_MAX_NODES];
   __shared__ double red_s[kWalkWaves];
-  __shared__ double node_s[3];  // M, Z, QS of the current node
+  __shared__ double node_s[4];  // M, Z, QS, and the residual mass at g = 1, of the current node
+  __shared__ double2 mass_s[LTD_SAMPLING_MAX_CHUNKS];  // the node's chunk masses at g = 0, 1
   __shared__ double target_s;  // the bonus search: mass left to pass in [lo_s, hi_s)
   __shared__ int lo_s, hi_s;
   if (halted(status)) return;
@@ -294,39 +412,18 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
   int bonus = 0;
   for (;;) {
     const int64_t row = (nb + u) * Voc;
-    // the node's softmax normaliser and draft sum from the chunk partials
+    // the node's softmax normaliser and draft sum from the chunk partials,
+    // and its chunk masses at g = 0 and g = 1
     if (w == 0) {
-      const NodeStats st = ws[(nb + u) * chunks + min(lane, chunks - 1)];
-      const float m_l = lane < chunks ? st.m : -INFINITY;
-      float Mf = m_l;
-      Mf = fmaxf(Mf, lane_xor_f<32>(Mf, lane));
-      Mf = fmaxf(Mf, lane_xor_f<16>(Mf, lane));
-      Mf = fmaxf(Mf, lane_xor_f<8>(Mf, lane));
-      Mf = fmaxf(Mf, lane_xor_f<4>(Mf, lane));
-      Mf = fmaxf(Mf, lane_xor_f<2>(Mf, lane));
-      Mf = fmaxf(Mf, lane_xor_f<1>(Mf, lane));
-      double zl = m_l != -INFINITY ? static_cast<double>(st.z) * exp(static_cast<double>(m_l - Mf)) : 0.0;
-      double ql = lane < chunks ? static_cast<double>(st.qs) : 0.0;
-#pragma unroll
-      for (int d = 32; d >= 1; d >>= 1) {
-        uint64_t oz, oq;
-        const uint64_t bz = static_cast<uint64_t>(__double_as_longlong(zl));
-        const uint64_t bq = static_cast<uint64_t>(__double_as_longlong(ql));
-        switch (d) {
-          case 32: oz = lane_xor_u64<32>(bz, lane); oq = lane_xor_u64<32>(bq, lane); break;
-          case 16: oz = lane_xor_u64<16>(bz, lane); oq = lane_xor_u64<16>(bq, lane); break;
-          case 8: oz = lane_xor_u64<8>(bz, lane); oq = lane_xor_u64<8>(bq, lane); break;
-          case 4: oz = lane_xor_u64<4>(bz, lane); oq = lane_xor_u64<4>(bq, lane); break;
-          case 2: oz = lane_xor_u64<2>(bz, lane); oq = lane_xor_u64<2>(bq, lane); break;
-          default: oz = lane_xor_u64<1>(bz, lane); oq = lane_xor_u64<1>(bq, lane);
-        }
-        zl += __longlong_as_double(static_cast<long long>(oz));
-        ql += __longlong_as_double(static_cast<long long>(oq));
-      }
+      const NodeTotals nt = merge_node_stats(ws + (nb + u) * chunks, chunks, lane);
+      const double2 ms = mass[(nb + u) * chunks + min(lane, chunks - 1)];
+      if (lane < chunks) mass_s[lane] = ms;
+      const double m1 = wave_sum_d(lane < chunks ? ms.y : 0.0, lane);
       if (lane == 0) {
-        node_s[0] = Mf;
-        node_s[1] = zl;
-        node_s[2] = ql;
+        node_s[0] = nt.Mf;
+        node_s[1] = nt.Z;
+        node_s[2] = nt.QS;
+        node_s[3] = m1;
       }
     }
     // the node's children, in ascending order, as bits of 64-node words
@@ -336,14 +433,12 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
       if (lane == 0) child_s[w] = m;
     }
     __syncthreads();
-    const float Mf = static_cast<float>(node_s[0]);
-    const double Z = node_s[1];
-    const double QS = node_s[2];
-    constexpr double kLog2e = 1.4426950408889634;
-    Residual res;
-    res.a = static_cast<float>(kLog2e * static_cast<double>(inv_t));
-    res.b = static_cast<float>(kLog2e * (static_cast<double>(Mf) + log(Z)));
-    res.gq = 0.f;
+    const NodeTotals nt{static_cast<float>(node_s[0]), node_s[1], node_s[2]};
+    const float Mf = nt.Mf;
+    const double Z = nt.Z;
+    const double QS = nt.QS;
+    const double mass_g1 = node_s[3];
+    Residual res = residual_params(nt, inv_t, 0.0);
 
     double g = 0.0, s = 1.0, D = 0.0;  // the residual after the rejections so far
     int n_removed = 0;
@@ -366,11 +461,18 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
           next = c;
           break;
         }
-        // rejected: the next residual needs one pass over the vocabulary
+        // rejected: the next residual's mass.  After the first rejection g is
+        // exactly 1 and the mass table holds it; later ones take one pass
+        // over the vocabulary.
         const double g2 = g + s / (1.0 - D);
-        res.gq = QS > 0.0 ? static_cast<float>(g2 / QS) : 0.f;
-        const float part = residual_pass(logits + row, draft_probs + row, Voc, t, res);
-        const double s2 = block_sum(static_cast<double>(part), red_s, lane, w);
+        double s2;
+        if (n_removed == 0) {
+          s2 = mass_g1;
+        } else {
+          res = residual_params(nt, inv_t, g2);
+          const float part = residual_pass(logits + row, draft_probs + row, Voc, t, res);
+          s2 = block_sum(static_cast<double>(part), red_s, lane, w);
+        }
         if (t == 0) removed_s[n_removed] = x;
         __syncthreads();
         if (!removed) D += Qx;
@@ -397,11 +499,48 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
     // target.  Where rounding leaves the target at or past a level's sum, the
     // last segment (token) with mass is taken, as the plain scan would.
     const bool use_q = g > 0.0;
-    res.gq = use_q && QS > 0.0 ? static_cast<float>(g / QS) : 0.f;
+    res = residual_params(nt, inv_t, g);
     const bool vec = (Voc & 3) == 0 && (reinterpret_cast<uintptr_t>(logits + row) & 15) == 0 &&
                      (reinterpret_cast<uintptr_t>(draft_probs + row) & 15) == 0;
     int lo = 0, hi = Voc;
     bool first = true;  // no level yet: the final scan sets the target itself
+    if (g == 0.0 || g == 1.0) {  // the first level from the mass table's chunks
+      if (t == 0) {
+        const bool g1 = g == 1.0;
+        double total = 0.0;
+        for (int c = 0; c < chunks; ++c) total += g1 ? mass_s[c].y : mass_s[c].x;
+        const double target = static_cast<double>(uniforms[(nb + u) * 2 + 1]) * total;
+        int pick = -1, last = -1;
+        double cum = 0.0, before = 0.0, upto_last = 0.0, run = 0.0;
+        for (int c = 0; c < chunks && pick < 0; ++c) {
+          const double mc = g1 ? mass_s[c].y : mass_s[c].x;
+          if (mc > 0.0) {
+            last = c;
+            upto_last = run;
+          }
+          before = cum;
+          cum += mc;
+          run = cum;
+          if (cum > target && mc > 0.0) pick = c;
+        }
+        if (pick < 0) {  // past the end by rounding (or no mass at all)
+          pick = last;
+          before = upto_last;
+        }
+        if (pick < 0) {
+          lo_s = 0;
+          hi_s = 0;  // no mass: token 0
+        } else {
+          lo_s = pick * kChunk;
+          hi_s = min(lo_s + kChunk, Voc);
+        }
+        target_s = target - before;
+      }
+      __syncthreads();
+      lo = lo_s;
+      hi = hi_s;
+      first = false;
+    }
     for (; hi - lo > kWave; first = false) {
       const int span = hi - lo;
       const int seg = vec ? ((span + 4 * kWalkWaves - 1) / (4 * kWalkWaves)) * 4
@@ -490,7 +629,8 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
 int sampling_chunks(int Voc) { return (Voc + kChunk - 1) / kChunk; }
 
 size_t sampling_workspace_bytes(int B, int Nmax, int Voc) {
-  return sizeof(NodeStats) * static_cast<size_t>(B) * Nmax * sampling_chunks(Voc);
+  return (sizeof(NodeStats) + sizeof(double2)) * static_cast<size_t>(B) * Nmax *
+         sampling_chunks(Voc);
 }
 
 hipError_t launch_sampling(const float* logits, const float* draft_probs,
@@ -501,12 +641,15 @@ hipError_t launch_sampling(const float* logits, const float* draft_probs,
                            const int32_t* status, hipStream_t stream) {
   const int chunks = sampling_chunks(Voc);
   auto* ws = static_cast<NodeStats*>(workspace);
+  auto* mass = reinterpret_cast<double2*>(ws + static_cast<size_t>(B) * Nmax * chunks);
   const float inv_t = 1.0f / temperature;
   hipLaunchKernelGGL(sample_stats_kernel, dim3(chunks, Nmax, B), dim3(kStatThreads), 0, stream,
                      logits, draft_probs, parents, n_nodes, Nmax, Voc, inv_t, ws, status);
+  hipLaunchKernelGGL(sample_mass_kernel, dim3(chunks, Nmax, B), dim3(kStatThreads), 0, stream,
+                     logits, draft_probs, parents, n_nodes, Nmax, Voc, inv_t, ws, mass, status);
   hipLaunchKernelGGL(sample_walk_kernel, dim3(B), dim3(kWalkThreads), 0, stream, logits,
                      draft_probs, draft_tokens, parents, n_nodes, uniforms, Nmax, Voc, inv_t, ws,
-                     chunks, accepted_nodes, out_tokens, n_accepted, status);
+                     mass, chunks, accepted_nodes, out_tokens, n_accepted, status);
   return hipGetLastError();
 }
 
