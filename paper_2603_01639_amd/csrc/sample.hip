@@ -14,17 +14,24 @@
 //     s_{k+1} = sum_v max(P(v) - g_{k+1} Q(v), 0)   (kept if it is 0).
 // So an accept test needs only P(x) and Q(x) and two scalars, each rejection
 // one pass over the vocabulary for s_{k+1}, and the bonus one inverse-CDF pass.
+// The first rejection at any node sets g_2 = 1 exactly, so the masses at g = 0
+// and g = 1 can be taken for every node at once, before the walk.
 //
 //   sample_stats_kernel  grid (vocab chunks of 4096, Nmax, B): per node, the
 //                        chunk's partial of the softmax of logits / T (max and
 //                        sum of exp) and, for nodes with children, the sum of
 //                        its draft row;
+//   sample_mass_kernel   the same grid: per node and chunk, the residual mass
+//                        at g = 0 and (nodes with children) g = 1, with the
+//                        walk's own parameters;
 //   sample_walk_kernel   one 1024-thread workgroup per sequence walks the tree:
-//                        scalar accept tests, a block-wide pass per rejection,
-//                        and for the bonus a search that narrows the range
-//                        holding the target mass sixteenfold per level (one
-//                        coalesced segment sum per wave), then a wave scan of
-//                        the last 64 tokens or fewer.
+//                        scalar accept tests; a node's first rejection reads
+//                        its mass from the table, each later one takes a
+//                        block-wide pass; the bonus takes its chunk from the
+//                        table when g is 0 or 1, and otherwise narrows the
+//                        range holding the target mass sixteenfold per level
+//                        (one coalesced segment sum per wave); a wave scan of
+//                        the last 64 tokens or fewer ends the search.
 // Element arithmetic is float32, every sum over the vocabulary is finished in
 // double.
 #include "ltd_device.hpp"
