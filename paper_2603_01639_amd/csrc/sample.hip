@@ -21,9 +21,10 @@
 //                        chunk's partial of the softmax of logits / T (max and
 //                        sum of exp) and, for nodes with children, the sum of
 //                        its draft row;
-//   sample_mass_kernel   the same grid: per node and chunk, the residual mass
-//                        at g = 0 and (nodes with children) g = 1, with the
-//                        walk's own parameters;
+//   sample_mass_kernel   the same grid, nodes with children only: per chunk,
+//                        the residual mass at g = 1 with the walk's own
+//                        parameters (the mass at g = 0 is the chunk's softmax
+//                        partial);
 //   sample_walk_kernel   one 1024-thread workgroup per sequence walks the tree:
 //                        scalar accept tests; a node's first rejection reads
 //                        its mass from the table, each later one takes a
@@ -47,6 +48,12 @@ constexpr int kWalkThreads = 1024;
 constexpr int kWalkWaves = kWalkThreads / kWave;
 constexpr int kMaxChunks = LTD_SAMPLING_MAX_CHUNKS;
 static_assert(kMaxChunks <= kWave, "the walk merges one chunk partial a lane");
+
+// Node j's parent as every kernel here reads it: in [0, j - 1] (the links of
+// a valid tree; malformed ones are clamped, so all kernels agree on the tree).
+__device__ __forceinline__ int link(const int32_t* __restrict__ parents, int64_t nb, int j) {
+  return j == 0 ? -1 : min(max(parents[nb + j], 0), j - 1);
+}
 
 struct NodeStats {  // per (sequence, node, chunk)
   float m;   // max of logits / T over the chunk
@@ -80,7 +87,7 @@ __global__ void __launch_bounds__(kStatThreads) sample_stats_kernel(
   if (t == 0) has_child_s = 0;
   __syncthreads();
   for (int j = t; j < n; j += kStatThreads)
-    if (parents[static_cast<int64_t>(b) * Nmax + j] == i && j > i) has_child_s = 1;
+    if (j > i && link(parents, static_cast<int64_t>(b) * Nmax, j) == i) has_child_s = 1;
   __syncthreads();
   const bool want_q = has_child_s != 0;
 #pragma unroll
@@ -317,18 +324,18 @@ __device__ double wave_range_sum(const float* __restrict__ l, const float* __res
   return wave_sum_d(acc, lane);
 }
 
-// Per (node, chunk): the residual mass sum_v max(P(v) - g Q(v), 0) over the
-// chunk at g = 0 (the softmax mass) and, for nodes with children, at g = 1
-// (after the node's first rejection, g is exactly 1), with the walk's own
-// parameters and element arithmetic.
+// Per (node with children, chunk): the residual mass
+// sum_v max(P(v) - Q(v), 0) over the chunk, i.e. at g = 1 (after the node's
+// first rejection, g is exactly 1), with the walk's own parameters and element
+// arithmetic.
 __global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
     const float* __restrict__ logits, const float* __restrict__ draft_probs,
     const int32_t* __restrict__ parents, const int32_t* __restrict__ n_nodes, int Nmax, int Voc,
-    float inv_t, const NodeStats* __restrict__ ws, double2* __restrict__ mass,
+    float inv_t, const NodeStats* __restrict__ ws, double* __restrict__ mass1,
     const int32_t* status) {
   __shared__ NodeTotals nt_s;
   __shared__ int has_child_s;
-  __shared__ double red_s[2][kStatThreads / kWave];
+  __shared__ double red_s[kStatThreads / kWave];
   if (halted(status)) return;
   const int chunk = blockIdx.x, i = blockIdx.y, b = blockIdx.z;
   const int chunks = gridDim.x;
@@ -336,11 +343,6 @@ __global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
   const int n = min(max(n_nodes[b], 1), Nmax);
   if (i >= n) return;  // uniform for the block
   const int64_t nb = static_cast<int64_t>(b) * Nmax;
-  const int64_t row = (nb + i) * Voc;
-  const int base = chunk * kChunk;
-  float l[kPerThread];
-#pragma unroll
-  for (int k = 0; k < kPerThread; ++k) l[k] = logits[row + min(base + k * kStatThreads + t, Voc - 1)];
   if (t == 0) has_child_s = 0;
   if (w == 0) {
     const NodeTotals nt = merge_node_stats(ws + (nb + i) * chunks, chunks, lane);
@@ -348,47 +350,46 @@ __global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
   }
   __syncthreads();
   for (int j = t; j < n; j += kStatThreads)
-    if (parents[nb + j] == i && j > i) has_child_s = 1;
+    if (j > i && link(parents, nb, j) == i) has_child_s = 1;
   __syncthreads();
-  const bool want_q = has_child_s != 0;
-  float q[kPerThread];
-#pragma unroll
-  for (int k = 0; k < kPerThread; ++k)
-    q[k] = want_q ? draft_probs[row + min(base + k * kStatThreads + t, Voc - 1)] : 0.f;
-  const NodeTotals nt = nt_s;
-  const Residual r0 = residual_params(nt, inv_t, 0.0);
-  const Residual r1 = residual_params(nt, inv_t, 1.0);
-  double d0 = 0.0, d1 = 0.0;
+  if (has_child_s == 0) return;  // uniform: a leaf never rejects
+  const int64_t row = (nb + i) * Voc;
+  const int base = chunk * kChunk;
+  float l[kPerThread], q[kPerThread];
 #pragma unroll
   for (int k = 0; k < kPerThread; ++k) {
-    if (base + k * kStatThreads + t < Voc) {
-      d0 += static_cast<double>(residual_elem(l[k], 0.f, r0));
-      d1 += static_cast<double>(residual_elem(l[k], q[k], r1));
-    }
+    const int64_t v = row + min(base + k * kStatThreads + t, Voc - 1);
+    l[k] = logits[v];
+    q[k] = draft_probs[v];
   }
-  d0 = wave_sum_d(d0, lane);
+  const Residual r1 = residual_params(nt_s, inv_t, 1.0);
+  double d1 = 0.0;
+#pragma unroll
+  for (int k = 0; k < kPerThread; ++k)
+    if (base + k * kStatThreads + t < Voc) d1 += static_cast<double>(residual_elem(l[k], q[k], r1));
   d1 = wave_sum_d(d1, lane);
-  if (lane == 0) {
-    red_s[0][w] = d0;
-    red_s[1][w] = d1;
-  }
+  if (lane == 0) red_s[w] = d1;
   __syncthreads();
   if (t == 0) {
-    double a0 = 0.0, a1 = 0.0;
+    double a1 = 0.0;
 #pragma unroll
-    for (int k = 0; k < kStatThreads / kWave; ++k) {
-      a0 += red_s[0][k];
-      a1 += red_s[1][k];
-    }
-    mass[(nb + i) * chunks + chunk] = make_double2(a0, want_q ? a1 : 0.0);
+    for (int k = 0; k < kStatThreads / kWave; ++k) a1 += red_s[k];
+    mass1[(nb + i) * chunks + chunk] = a1;
   }
+}
+
+// Whether node u has a child, by one wave over the parent links in LDS.
+__device__ __forceinline__ bool child_any(const int32_t* par_s, int n, int u, int lane) {
+  bool any = false;
+  for (int j = u + 1 + lane; j < n; j += kWave) any = any || par_s[j] == u;
+  return __ballot(any) != 0;
 }
 
 __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
     const float* __restrict__ logits, const float* __restrict__ draft_probs,
     const int32_t* __restrict__ draft_tokens, const int32_t* __restrict__ parents,
     const int32_t* __restrict__ n_nodes, const float* __restrict__ uniforms, int Nmax, int Voc,
-    float inv_t, const NodeStats* __restrict__ ws, const double2* __restrict__ mass, int chunks,
+    float inv_t, const NodeStats* __restrict__ ws, const double* __restrict__ mass1, int chunks,
     int32_t* __restrict__ accepted, int32_t* __restrict__ out_tokens,
     int32_t* __restrict__ n_accepted, const int32_t* status) {
   __shared__ int32_t par_s[LTD_MAX_NODES];
@@ -407,8 +408,7 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
   const int n = min(max(n_nodes[b], 1), Nmax);
   const int64_t nb = static_cast<int64_t>(b) * Nmax;
   if (t < Nmax) {
-    const int32_t p = parents[nb + t];
-    par_s[t] = t == 0 || t >= n ? -1 : min(max(p, 0), t - 1);
+    par_s[t] = t >= n ? -1 : link(parents, nb, t);
     tok_s[t] = min(max(draft_tokens[nb + t], 0), Voc - 1);
   }
   __syncthreads();
@@ -420,12 +420,19 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
   for (;;) {
     const int64_t row = (nb + u) * Voc;
     // the node's softmax normaliser and draft sum from the chunk partials,
-    // and its chunk masses at g = 0 and g = 1
+    // and its chunk masses at g = 0 (the chunk's softmax mass, from its
+    // partial) and at g = 1 (the mass table; written for nodes with children)
     if (w == 0) {
       const NodeTotals nt = merge_node_stats(ws + (nb + u) * chunks, chunks, lane);
-      const double2 ms = mass[(nb + u) * chunks + min(lane, chunks - 1)];
-      if (lane < chunks) mass_s[lane] = ms;
-      const double m1 = wave_sum_d(lane < chunks ? ms.y : 0.0, lane);
+      const NodeStats st = ws[(nb + u) * chunks + min(lane, chunks - 1)];
+      const bool kids = child_any(par_s, n, u, lane);
+      const double m1c = kids ? mass1[(nb + u) * chunks + min(lane, chunks - 1)] : 0.0;
+      const double m0c = st.m != -INFINITY
+                             ? static_cast<double>(st.z) *
+                                   exp(static_cast<double>(st.m) - static_cast<double>(nt.Mf)) / nt.Z
+                             : 0.0;
+      if (lane < chunks) mass_s[lane] = make_double2(m0c, m1c);
+      const double m1 = wave_sum_d(lane < chunks ? m1c : 0.0, lane);
       if (lane == 0) {
         node_s[0] = nt.Mf;
         node_s[1] = nt.Z;
@@ -636,7 +643,7 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
 int sampling_chunks(int Voc) { return (Voc + kChunk - 1) / kChunk; }
 
 size_t sampling_workspace_bytes(int B, int Nmax, int Voc) {
-  return (sizeof(NodeStats) + sizeof(double2)) * static_cast<size_t>(B) * Nmax *
+  return (sizeof(NodeStats) + sizeof(double)) * static_cast<size_t>(B) * Nmax *
          sampling_chunks(Voc);
 }
 
@@ -648,15 +655,15 @@ hipError_t launch_sampling(const float* logits, const float* draft_probs,
                            const int32_t* status, hipStream_t stream) {
   const int chunks = sampling_chunks(Voc);
   auto* ws = static_cast<NodeStats*>(workspace);
-  auto* mass = reinterpret_cast<double2*>(ws + static_cast<size_t>(B) * Nmax * chunks);
+  auto* mass1 = reinterpret_cast<double*>(ws + static_cast<size_t>(B) * Nmax * chunks);
   const float inv_t = 1.0f / temperature;
   hipLaunchKernelGGL(sample_stats_kernel, dim3(chunks, Nmax, B), dim3(kStatThreads), 0, stream,
                      logits, draft_probs, parents, n_nodes, Nmax, Voc, inv_t, ws, status);
   hipLaunchKernelGGL(sample_mass_kernel, dim3(chunks, Nmax, B), dim3(kStatThreads), 0, stream,
-                     logits, draft_probs, parents, n_nodes, Nmax, Voc, inv_t, ws, mass, status);
+                     logits, draft_probs, parents, n_nodes, Nmax, Voc, inv_t, ws, mass1, status);
   hipLaunchKernelGGL(sample_walk_kernel, dim3(B), dim3(kWalkThreads), 0, stream, logits,
                      draft_probs, draft_tokens, parents, n_nodes, uniforms, Nmax, Voc, inv_t, ws,
-                     mass, chunks, accepted_nodes, out_tokens, n_accepted, status);
+                     mass1, chunks, accepted_nodes, out_tokens, n_accepted, status);
   return hipGetLastError();
 }
 
