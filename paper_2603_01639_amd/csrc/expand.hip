@@ -115,8 +115,6 @@ __device__ __forceinline__ uint32_t wave_nth_largest(uint32_t v, int n) {
   return t;
 }
 
-__device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
-
 // (m, z) pairs: z is a sum of exp(x - m).
 __device__ __forceinline__ void lse_combine(float& m, float& z, float m2, float z2) {
   const float mx = fmaxf(m, m2);
