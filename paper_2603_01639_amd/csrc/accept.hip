@@ -29,7 +29,6 @@ namespace {
 constexpr int kArgmaxThreads = 256;
 constexpr int kChunk = 8192;                                // logits per workgroup (32 KiB)
 constexpr int kVecPerThread = kChunk / 4 / kArgmaxThreads;  // 16-byte loads per thread
-constexpr int kVecInFlight = 4;  // loads per batch (measured: 4 beats 8 and 2)
 constexpr int kScanThreads = LTD_MAX_NODES;                 // one thread per node
 constexpr int kKeysPerRound = 8;                            // key loads in flight per thread
 constexpr int kLiftLevels = 8;                              // 2^8 = LTD_MAX_NODES
@@ -69,25 +68,31 @@ __global__ void __launch_bounds__(kArgmaxThreads) argmax_partial_kernel(
     const f32x4* row4 = reinterpret_cast<const f32x4*>(row);
     const int f0 = (lo >> 2) + threadIdx.x;
     const int fend = hi >> 2;
+    // All loads in flight at once; then the thread's float maximum, and the
+    // lowest index holding it (-0.0 == +0.0, and pack_key makes both +0.0),
+    // which is the thread's largest packed key: about three operations per
+    // element instead of a 64-bit key and maximum each.
+    f32x4 x[kVecPerThread];
 #pragma unroll
-    for (int u0 = 0; u0 < kVecPerThread; u0 += kVecInFlight) {
-      f32x4 x[kVecInFlight];
-#pragma unroll
-      for (int u = 0; u < kVecInFlight; ++u) {
-        const int f = f0 + (u0 + u) * kArgmaxThreads;
-        x[u] = f < fend ? __builtin_nontemporal_load(row4 + f) : (f32x4){0.f, 0.f, 0.f, 0.f};
-      }
-#pragma unroll
-      for (int u = 0; u < kVecInFlight; ++u) {
-        const int f = f0 + (u0 + u) * kArgmaxThreads;
-        if (f < fend) {
-          const int v = f << 2;
-          const uint64_t k01 = max_u64(pack_key(x[u].x, v), pack_key(x[u].y, v + 1));
-          const uint64_t k23 = max_u64(pack_key(x[u].z, v + 2), pack_key(x[u].w, v + 3));
-          best = max_u64(best, max_u64(k01, k23));
-        }
-      }
+    for (int u = 0; u < kVecPerThread; ++u) {
+      const int f = f0 + u * kArgmaxThreads;
+      x[u] = f < fend ? __builtin_nontemporal_load(row4 + f)
+                      : (f32x4){-INFINITY, -INFINITY, -INFINITY, -INFINITY};
     }
+    float vm = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kVecPerThread; ++u)
+      vm = fmaxf(vm, fmaxf(fmaxf(x[u].x, x[u].y), fmaxf(x[u].z, x[u].w)));
+    int bi = 0x7FFFFFFF;
+#pragma unroll
+    for (int u = kVecPerThread - 1; u >= 0; --u) {  // downwards: the lowest index wins
+      const int v = (f0 + u * kArgmaxThreads) << 2;
+      bi = x[u].w == vm ? v + 3 : bi;
+      bi = x[u].z == vm ? v + 2 : bi;
+      bi = x[u].y == vm ? v + 1 : bi;
+      bi = x[u].x == vm ? v : bi;
+    }
+    if (bi < hi) best = pack_key(vm, bi);  // (padding past the row is never the lowest)
   } else {
     for (int v = lo + threadIdx.x; v < hi; v += kArgmaxThreads) best = max_u64(best, pack_key(row[v], v));
   }
