@@ -206,8 +206,7 @@ struct NodeTotals {
   float Mf;
   double Z, QS;
 };
-__device__ NodeTotals merge_node_stats(const NodeStats* __restrict__ st_row, int chunks, int lane) {
-  const NodeStats st = st_row[min(lane, chunks - 1)];
+__device__ NodeTotals merge_node_stats_of(const NodeStats st, int chunks, int lane) {
   const float m_l = lane < chunks ? st.m : -INFINITY;
   float Mf = m_l;
   Mf = fmaxf(Mf, lane_xor_f<32>(Mf, lane));
@@ -236,6 +235,9 @@ __device__ NodeTotals merge_node_stats(const NodeStats* __restrict__ st_row, int
     ql += __longlong_as_double(static_cast<long long>(oq));
   }
   return NodeTotals{Mf, zl, ql};
+}
+__device__ NodeTotals merge_node_stats(const NodeStats* __restrict__ st_row, int chunks, int lane) {
+  return merge_node_stats_of(st_row[min(lane, chunks - 1)], chunks, lane);
 }
 
 constexpr double kLog2e = 1.4426950408889634;
@@ -352,7 +354,10 @@ __global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
   for (int j = t; j < n; j += kStatThreads)
     if (j > i && link(parents, nb, j) == i) has_child_s = 1;
   __syncthreads();
-  if (has_child_s == 0) return;  // uniform: a leaf never rejects
+  if (has_child_s == 0) {  // uniform: a leaf never rejects; its entry reads as 0
+    if (t == 0) mass1[(nb + i) * chunks + chunk] = 0.0;
+    return;
+  }
   const int64_t row = (nb + i) * Voc;
   const int base = chunk * kChunk;
   float l[kPerThread], q[kPerThread];
@@ -423,10 +428,12 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
     // and its chunk masses at g = 0 (the chunk's softmax mass, from its
     // partial) and at g = 1 (the mass table; written for nodes with children)
     if (w == 0) {
-      const NodeTotals nt = merge_node_stats(ws + (nb + u) * chunks, chunks, lane);
+      // both loads first (a leaf's mass entries are 0)
       const NodeStats st = ws[(nb + u) * chunks + min(lane, chunks - 1)];
+      const double m1_any = mass1[(nb + u) * chunks + min(lane, chunks - 1)];
+      const NodeTotals nt = merge_node_stats_of(st, chunks, lane);
       const bool kids = child_any(par_s, n, u, lane);
-      const double m1c = kids ? mass1[(nb + u) * chunks + min(lane, chunks - 1)] : 0.0;
+      const double m1c = kids ? m1_any : 0.0;
       const double m0c = st.m != -INFINITY
                              ? static_cast<double>(st.z) *
                                    exp(static_cast<double>(st.m) - static_cast<double>(nt.Mf)) / nt.Z
