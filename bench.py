@@ -1,6 +1,9 @@
 """Benchmark: one tree-verification step (tree attention + greedy acceptance +
 KV compaction) on one MI355X, on synthetic inputs shaped like the paper's
-Llama-3-8B verification workload.
+workloads.  The default workload is the largest one that fits a GPU: 16
+sequences with 70B-shaped attention (64 q / 8 kv heads, head_dim 128, bf16),
+prefixes of 1024-8192 tokens in a paged cache of 16-token blocks, and draft
+trees of 16-128 nodes.
 
     python bench.py [--steps K] [--warmup W] [--workload c2|c3|c4|c5] [--no-cpu-baseline]
 
@@ -13,6 +16,11 @@ reads cold data.  `eager_us` is the same K steps launched one by one from
 Python.  `roofline` describes the dominant call: algorithmic bytes per launch
 over its average duration (a graph of K such calls, timed the same way).
 `cpu_baseline` times the CPU oracle on the host on a bounded sample.
+
+`attention_by_workload` times the attention call alone, the same way, on the
+other workloads: the 8B-shaped step at prefix 2048 and 16384 (HBM-bound) and
+the 32B-shaped sweep over tree sizes N = 8 .. 256 at prefix 4096, each with
+its binding roof and fraction.
 
 The steps before verification are timed apart the same way and reported
 under `kernels`, not in `value`: acceptance at temperature 1 on the 8B-shaped
@@ -37,6 +45,9 @@ import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
+# the seeded input generator lives with the tests (it is shared by the
+# benchmark, the tests and the smoke check, and by nothing in the package)
+sys.path.insert(0, os.path.join(ROOT, "tests"))
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, datasheet
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
@@ -50,10 +61,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="c2", choices=["c2", "c3", "c4", "c5"])
+    ap.add_argument("--workload", default="c5", choices=["c2", "c3", "c4", "c5"])
     ap.add_argument("--c4-n", type=int, default=64)
     ap.add_argument("--c4-depth", type=int, default=6)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra-workloads", action="store_true",
+                    help="skip the attention-only timings of the other workloads")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic.txt"),
                     help="measured HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE summary)")
@@ -61,7 +74,7 @@ def parse():
 
 
 def make_workload(args):
-    from paper_2603_01639_amd import workloads as W
+    import workloads as W
     if args.workload == "c2":
         b = W.config2_8b(0)
         desc = ("Llama-3-8B-shaped bf16 tree verify: batch 1, 32 q / 8 kv heads, head_dim 128, "
@@ -83,7 +96,7 @@ def make_workload(args):
 
 def select_workload(name):
     """Candidate pools shaped like each verify workload's trees."""
-    from paper_2603_01639_amd import workloads as W
+    import workloads as W
     return {"c2": W.select_8b, "c3": W.select_8b, "c4": W.select_deep,
             "c5": W.select_batch16}[name](0)
 
@@ -300,7 +313,7 @@ def main():
 
     # ---- acceptance at T = 1 (recursive rejection sampling) on the 8B-shaped
     # tree, in place of greedy acceptance (a graph of K calls)
-    from paper_2603_01639_amd import workloads as W
+    import workloads as W
     smp = W.sampling_8b(0)
     s_in = [to_dev(a) for a in (smp.logits, smp.draft_probs, smp.draft_tokens, smp.parents,
                                 smp.n_nodes, smp.uniforms)]
@@ -329,7 +342,7 @@ def main():
 
     # ---- draft policies, outside the step (graphs of K calls), one state
     # per sequence of the workload
-    from paper_2603_01639_amd import workloads as W
+    import workloads as W
     for layout, name in ((W.LAYOUT_SIZE, "size_policy"), (W.LAYOUT_DEPTH, "depth_policy")):
         pb = W.policy_batch(layout, b.B)
         layers = [(to_dev(w), to_dev(bias)) for w, bias in pb.layers]
@@ -355,12 +368,16 @@ def main():
                          "weight_bytes": wbytes,
                          "GB/s": round(wbytes / (p_us * 1e-6) / 1e9, 1), "in_value": False}
     dom = max(("tree_verify_attn", "tree_accept"), key=lambda n: per_call_us[n])
-    traffic = read_traffic(args.traffic, args.workload, dom)
+    traffic = read_traffic(args.traffic, workload_key(args.workload, args.c4_n), dom)
     roof = binding_roof(dom, kernels[dom]["alg_bytes"],
                         flops if dom == "tree_verify_attn" else 0, per_call_us[dom])
     roof.update({"traffic": traffic, "hbm_GBps": kernels[dom]["GB/s"],
                  "copy_GBps": round(copy_gbs, 1),
                  "hbm_frac_of_copy": round(kernels[dom]["GB/s"] / copy_gbs, 4)})
+
+    extra = None
+    if not args.no_extra_workloads:
+        extra = attention_by_workload(ltd, torch, to_dev, args, graph_of, timed, stream)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -388,7 +405,69 @@ def main():
         "kernels": kernels,
         "cpu_baseline": cpu,
     }
+    if extra is not None:
+        rec["attention_by_workload"] = extra
     print(json.dumps(rec), flush=True)
+
+
+EXTRA_WORKLOADS = [("c2", None), ("c3", None)] + [("c4", n) for n in (8, 16, 32, 64, 128, 256)]
+
+
+def workload_key(name, c4_n=None):
+    """The name a workload's counters are filed under in the traffic summary."""
+    return f"c4n{c4_n}" if name == "c4" else name
+
+
+def attention_by_workload(ltd, torch, to_dev, args, graph_of, timed, stream):
+    """The attention call alone on the other workloads (c4 at depth 6), timed
+    like the main one: a graph of K calls over rotated input copies (> 2x the
+    Infinity Cache, so every call reads cold K/V), replayed once between
+    events on the launch stream."""
+    import workloads as W
+    out_rows = {}
+    steps = max(20, min(args.steps, 100))
+    for name, n in EXTRA_WORKLOADS:
+        if name == args.workload and (name != "c4" or n == args.c4_n):
+            continue
+        if name == "c2":
+            b = W.config2_8b(0, with_logits=False)
+        elif name == "c3":
+            b = W.config3_long(0, with_logits=False)
+        else:
+            b = W.config4_sweep(n, min(6, n), with_logits=False)
+        attn_bytes, _, flops = algorithmic_bytes(b)
+        per_copy = b.k_cache.nbytes + b.v_cache.nbytes + b.q.nbytes
+        copies = max(2, min(32, math.ceil(2.2 * MALL_BYTES / per_copy)))
+        shared = [to_dev(a) for a in (b.prefix_len, b.parents, b.n_nodes)]
+        sets = [[to_dev(b.q), to_dev(b.k_cache), to_dev(b.v_cache)] for _ in range(copies)]
+        out = torch.empty(tuple(b.q.shape), dtype=sets[0][0].dtype, device="cuda")
+        ws = torch.empty(max(1, ltd.attn_workspace_size(b.B, b.Nmax, b.Hq, b.Hkv, b.d,
+                                                        b.max_prefix, b.dtype)),
+                         dtype=torch.uint8, device="cuda")
+        torch.cuda.synchronize()
+
+        def call(i, sets=sets, shared=shared, out=out, ws=ws, b=b):
+            q, k, v = sets[i % len(sets)]
+            ltd.tree_verify_attn(q, k, v, *shared, out, max_prefix=b.max_prefix, workspace=ws,
+                                 stream=stream)
+
+        for i in range(3):
+            call(i)
+        g = graph_of(call, steps)
+        us = 1e3 * timed(lambda i: g.replay(), 1) / steps
+        del g
+        key = workload_key(name, n)
+        roof = binding_roof("tree_verify_attn", attn_bytes, flops, us)
+        roof["us"] = round(us, 3)
+        roof["alg_bytes"] = attn_bytes
+        roof["alg_flops"] = flops
+        roof["traffic"] = read_traffic(args.traffic, key, "tree_verify_attn")
+        roof["shape"] = (f"B={b.B} Hq={b.Hq} Hkv={b.Hkv} d={b.d} P={int(b.prefix_len[0])} "
+                         f"N={int(b.n_nodes[0])}")
+        out_rows[key] = roof
+        del sets, out, ws
+        torch.cuda.synchronize()
+    return out_rows
 
 
 def binding_roof(call, alg_bytes, alg_flops, us):
@@ -407,7 +486,7 @@ def binding_roof(call, alg_bytes, alg_flops, us):
 
 # The kernel sources behind each call's counters (launch plan included).
 CALL_SOURCES = {
-    "tree_verify_attn": ("attn_mfma.hip", "attn_plan.hip", "attn_rowwise.hip", "ltd_device.hpp"),
+    "tree_verify_attn": ("attn_mfma.hip", "attn_plan.hip", "ltd_device.hpp"),
     "tree_accept": ("accept.hip", "ltd_device.hpp"),
 }
 
@@ -435,33 +514,51 @@ def read_traffic(path, workload, call):
     return None
 
 
+def first_sequence(b):
+    """The batch cut down to its first sequence (a paged cache keeps its whole
+    block pool; only the blocks sequence 0's table names are read)."""
+    import dataclasses
+    one = dict(q=b.q[:1], prefix_len=b.prefix_len[:1], parents=b.parents[:1],
+               n_nodes=b.n_nodes[:1], draft_tokens=b.draft_tokens[:1],
+               logits=None if b.logits is None else b.logits[:1], B=1)
+    if b.block_table is not None:
+        one["block_table"] = b.block_table[:1]
+    else:
+        one["k_cache"], one["v_cache"] = b.k_cache[:1], b.v_cache[:1]
+    return dataclasses.replace(b, **one)
+
+
 def cpu_baseline(b, seconds):
-    """The CPU oracle (fp64 C, OpenMP) on whole verify steps of the same
-    workload, repeated for about `seconds` of wall time."""
+    """The CPU oracle (fp64 C, OpenMP over every host core) on whole verify
+    steps of the same workload, repeated for about `seconds` of wall time (at
+    least one step).  The one-core figure is taken on a bounded sample: the
+    first sequence's step on one thread, scaled to the whole batch by its share
+    of the attention FLOPs (the attention is nearly all of the oracle's work)."""
     import oracle
 
-    def one_step():
-        oracle.tree_verify_attn(b.q, b.k_cache, b.v_cache, b.prefix_len, b.parents, b.n_nodes,
-                                Hkv=b.Hkv, block_table=b.block_table, num_blocks=b.num_blocks,
-                                dtype=b.dtype)
-        _, acc, _, nacc = oracle.tree_accept(b.logits, b.draft_tokens, b.parents, b.n_nodes)
-        k, v = b.k_cache.copy(), b.v_cache.copy()
-        oracle.kv_compact(k, v, b.prefix_len, acc, nacc, Hkv=b.Hkv, block_table=b.block_table,
-                          num_blocks=b.num_blocks)
+    def one_step(bb):
+        oracle.tree_verify_attn(bb.q, bb.k_cache, bb.v_cache, bb.prefix_len, bb.parents,
+                                bb.n_nodes, Hkv=bb.Hkv, block_table=bb.block_table,
+                                num_blocks=bb.num_blocks, dtype=bb.dtype)
+        _, acc, _, nacc = oracle.tree_accept(bb.logits, bb.draft_tokens, bb.parents, bb.n_nodes)
+        k, v = bb.k_cache.copy(), bb.v_cache.copy()
+        oracle.kv_compact(k, v, bb.prefix_len, acc, nacc, Hkv=bb.Hkv,
+                          block_table=bb.block_table, num_blocks=bb.num_blocks)
 
     reps, t_start = 0, time.perf_counter()
     while True:
-        one_step()
+        one_step(b)
         reps += 1
         el = time.perf_counter() - t_start
         if el >= seconds or reps >= 1000:
             break
     cores = oracle.num_threads()
-    # the same step on one core, a few repetitions
+    b1 = first_sequence(b)
+    share = algorithmic_bytes(b1)[2] / max(1, algorithmic_bytes(b)[2])
     oracle.set_num_threads(1)
     one_reps, t1 = 0, time.perf_counter()
     while True:
-        one_step()
+        one_step(b1)
         one_reps += 1
         el1 = time.perf_counter() - t1
         if el1 >= min(seconds, 6.0) or one_reps >= 1000:
@@ -477,9 +574,11 @@ def cpu_baseline(b, seconds):
         pass
     return {"value": round(el / reps * 1e6, 1), "unit": "µs", "cores": cores,
             "kind": "oracle",
-            "sample": f"{reps} whole verify steps of the benchmark workload (attention for every "
+            "sample": f"{reps} whole verify step(s) of the benchmark workload (attention for every "
                       f"node and head, acceptance, compaction incl. a cache copy), fp64 C oracle",
-            "one_core_value": round(el1 / one_reps * 1e6, 1), "one_core_steps": one_reps,
+            "one_core_value": round(el1 / one_reps / share * 1e6, 1),
+            "one_core_sample": f"{one_reps} step(s) of the first sequence alone on one thread "
+                               f"({share:.3f} of the batch's attention FLOPs), scaled to the batch",
             "cpu_model": model}
 
 

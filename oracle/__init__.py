@@ -70,10 +70,11 @@ def load_library(path: str) -> ctypes.CDLL:
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
+        path = os.environ.get("LTD_ORACLE_LIB") or LIB_PATH  # e.g. the sanitizer build
+        if not os.path.exists(path):
             from . import build as _build
             _build.build()
-        _lib = load_library(LIB_PATH)
+        _lib = load_library(path)
     return _lib
 
 

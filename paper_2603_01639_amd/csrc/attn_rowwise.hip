@@ -9,6 +9,7 @@
 // mask shows each candidate its ancestors only).
 #include "ltd_device.hpp"
 #include "ltd_launch.hpp"
+#include "tree_walk.hpp"
 
 namespace ltd {
 namespace {
@@ -38,11 +39,7 @@ __global__ void __launch_bounds__(kWave) attn_rowwise_kernel(
 
   const int64_t q_off = ((static_cast<int64_t>(b) * Nmax + i) * Hq + h) * d;
   for (int e = lane; e < d; e += kWave) q_s[e] = load_f32(q, q_off + e) * scale;
-  if (lane == 0) {  // root path of node i (tree rows it may see)
-    int len = 0;
-    for (int j = i; j != -1; j = par[j]) path_s[len++] = j;
-    path_len_s = len;
-  }
+  if (lane == 0) path_len_s = root_path(par, i, path_s);  // tree rows node i may see
   __syncthreads();
   const int n_keys = P + path_len_s;
 

@@ -8,7 +8,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
 import bench  # noqa: E402
-from paper_2603_01639_amd import workloads as W  # noqa: E402
+import workloads as W  # noqa: E402
 
 
 def test_binding_roof_hbm_and_mfma():

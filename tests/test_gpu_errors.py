@@ -7,7 +7,7 @@ import pytest
 
 import gpu_util as U
 import paper_2603_01639_amd as ltd
-from paper_2603_01639_amd import workloads as W
+import workloads as W
 
 pytestmark = pytest.mark.gpu
 

@@ -14,7 +14,7 @@ import pytest
 import gpu_util as U
 from oracle import policy as OP
 import paper_2603_01639_amd as ltd
-from paper_2603_01639_amd import workloads as W
+import workloads as W
 
 pytestmark = pytest.mark.gpu
 

@@ -16,7 +16,7 @@ import pytest
 import gpu_util as U
 import oracle
 import paper_2603_01639_amd as ltd
-from paper_2603_01639_amd import workloads as W
+import workloads as W
 import test_oracle_sampling as TS
 
 pytestmark = pytest.mark.gpu

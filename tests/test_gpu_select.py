@@ -10,7 +10,7 @@ import gpu_util as U
 import oracle
 import paper_2603_01639_amd as ltd
 import test_oracle_select as TS
-from paper_2603_01639_amd import workloads as W
+import workloads as W
 
 pytestmark = pytest.mark.gpu
 

@@ -17,7 +17,7 @@ import torch
 
 import oracle
 from brute import all_parent_arrays, ancestor_mask_closure, attention_by_root_path
-from paper_2603_01639_amd import workloads as W
+import workloads as W
 
 F32 = oracle.DTYPE_F32
 BF16 = oracle.DTYPE_BF16

@@ -18,7 +18,7 @@ import numpy as np
 import pytest
 
 import oracle
-from paper_2603_01639_amd import workloads as W
+import workloads as W
 
 
 def _empty_pool(B, Vpool):

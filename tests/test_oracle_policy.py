@@ -95,3 +95,70 @@ def test_state_layouts():
     assert s.tolist() == [[4, 2048, 0, -1, -2, -3], [2, 77, 0, -0.5, -50, -50]]
     s = OP.policy_state(OP.LAYOUT_DEPTH, scores, size, D, L, 3, -50.0)
     assert s.tolist() == [[-2, -3, -4, 4, 2048], [-50, 0, -0.5, 2, 77]]
+
+
+# ------------------------------------------------- the rounding-bound network
+# policy_mlp_abs feeds the GPU test's tolerance: sum(in widths) * 2^-24 * the
+# network evaluated on |x|, |W|, |b| without clipping (the first-order bound on
+# the rounding error of float32 dot products accumulated in any order).
+
+def test_abs_network_worked_example():
+    """By hand: |x| = [1, 2]; layer 1 gives [1*1 + 1*2 + 1, 3*1 + 2*2 + 0.5] =
+    [4, 7.5]; layer 2 gives 2*4 + 1*7.5 + 4 = 19.5."""
+    layers = [(np.array([[1.0, -1.0], [-3.0, 2.0]]), np.array([-1.0, 0.5])),
+              (np.array([[2.0, -1.0]]), np.array([-4.0]))]
+    got = OP.policy_mlp_abs(np.array([[1.0, -2.0]]), layers)
+    assert got.tolist() == [[19.5]]
+
+
+def test_abs_network_bounds_every_partial_sum_and_is_tight():
+    rng = np.random.default_rng(5)
+    dims = [13, 17, 11, 5]
+    layers = random_layers(rng, dims)
+    x = rng.normal(size=(6, dims[0])) * 4
+    for k in range(len(layers)):
+        bound = OP.policy_mlp_abs(x, layers[:k + 1])
+        # the input of layer k, exactly
+        h = x if k == 0 else OP.policy_mlp(x, layers[:k] + [(np.eye(dims[k]), np.zeros(dims[k]))])[0]
+        w, b = (np.asarray(a, np.float64) for a in layers[k])
+        partial = np.cumsum(h[:, None, :] * w[None, :, :], axis=2) + b[None, :, None]
+        assert (np.abs(partial) <= bound[:, :, None] * (1 + 1e-12)).all(), k
+    # nonnegative inputs, weights and biases: no ReLU clips, the bound is the output
+    pos = [(np.abs(np.asarray(w, np.float64)), np.abs(np.asarray(b, np.float64))) for w, b in layers]
+    xp = np.abs(x)
+    np.testing.assert_allclose(OP.policy_mlp_abs(xp, pos), OP.policy_mlp(xp, pos)[0], rtol=1e-12)
+
+
+def _forward_f32(x, layers, order):
+    """Float32 forward pass with each dot product accumulated one term at a
+    time in the given order of the input index (the bias added last)."""
+    h = np.asarray(x, np.float32)
+    for k, (w, b) in enumerate(layers):
+        w = np.asarray(w, np.float32)
+        acc = np.zeros((h.shape[0], w.shape[0]), np.float32)
+        for j in order(w.shape[1]):
+            acc = (acc + h[:, j:j + 1] * w[None, :, j][0]).astype(np.float32)
+        acc = (acc + np.asarray(b, np.float32)).astype(np.float32)
+        h = np.maximum(acc, np.float32(0)) if k + 1 < len(layers) else acc
+    return h.astype(np.float64)
+
+
+@pytest.mark.parametrize("order", ["forward", "reverse", "strided"])
+def test_float32_forward_within_the_derived_tolerance(order):
+    """The tolerance the GPU test applies holds for float32 passes that sum in
+    different orders, and it is not vacuous: a pass that drops one input term
+    of every dot product (a loop bound off by one) breaks it."""
+    orders = {"forward": lambda n: range(n), "reverse": lambda n: range(n - 1, -1, -1),
+              "strided": lambda n: [j for r in range(8) for j in range(r, n, 8)],
+              "drop_last": lambda n: range(n - 1)}
+    rng = np.random.default_rng(11)
+    dims = [102, 256, 64, 12]
+    layers = random_layers(rng, dims)
+    x = rng.normal(size=(4, dims[0])) * 5
+    x32 = x.astype(np.float32).astype(np.float64)
+    exact = OP.policy_mlp(x32, layers)[0]
+    tol = sum(dims[:-1]) * 2.0 ** -24 * OP.policy_mlp_abs(x32, layers)
+    got = _forward_f32(x32, layers, orders[order])
+    assert (np.abs(got - exact) <= tol).all()
+    bad = _forward_f32(x32, layers, orders["drop_last"])
+    assert (np.abs(bad - exact) > tol).any()

@@ -27,7 +27,7 @@ import pytest
 
 import oracle
 from brute import all_parent_arrays, root_path
-from paper_2603_01639_amd import workloads as W
+import workloads as W
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "select_examples.json")
 

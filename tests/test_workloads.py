@@ -3,7 +3,7 @@ import numpy as np
 import pytest
 
 from brute import root_path
-from paper_2603_01639_amd import workloads as W
+import workloads as W
 
 
 def _levels(par):

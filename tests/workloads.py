@@ -1,12 +1,16 @@
 """Seeded synthetic inputs shaped like the paper's verification workloads.
 
-This module only *draws data*: draft pools and trees, tokens, queries, KV
-caches, target logits and paged block tables.  It contains none of the
-verification step's arithmetic (no attention, no argmax, no acceptance walk, no
-compaction), so the GPU path and the CPU oracle can both consume its arrays
-without sharing any of the method's code.  Trees for the verification inputs
-are cut from a draft pool by a short selection of the generator's own
-(``tree_eagle``); neither the GPU selection kernel nor the oracle uses it.
+Test infrastructure: the GPU parity tests, the oracle's pins, the smoke check
+and the benchmark draw their inputs here; nothing in the HIP library or the
+oracle imports it.  It computes none of the verification step itself (no
+attention, argmax, acceptance walk or compaction).  It does hold two pieces of
+the draft side of the method, written independently in numpy, because
+realistic trees need them: ``draft_pool`` runs the beam of section 3.2 ("Draft
+Tree Generation") on random draft distributions, and ``tree_eagle`` cuts a
+pool to its top-N candidates ("Candidate Token Selection").  The kernels only
+ever see their outputs (parents, tokens, scores); the oracle's selection and
+expansion are also checked against these two functions as independent
+implementations.
 
 Shapes follow the paper's setting (arXiv 2603.01639): Eagle-style beam trees of
 width W and depth D (section 3.2, "Draft Tree Generation"), a verification size
@@ -43,11 +47,18 @@ def config_seed(config: int, rep: int = 0) -> int:
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """Round float32 to bf16 (nearest, ties to even); return uint16 bits."""
-    x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    return rounded.astype(np.uint16)
+    """Round float32 to bf16 (nearest, ties to even); return uint16 bits.
+
+    In 32-bit integer arithmetic, in place on a copy: adding 0x7FFF plus the
+    kept part's lowest bit cannot wrap for any finite or infinite input (the
+    largest pattern, -inf = 0xFF800000, stays far below 2^32 - 0x8000)."""
+    u = np.array(x, dtype=np.float32, copy=True).view(np.uint32)
+    t = u >> 16
+    t &= 1
+    t += 0x7FFF
+    u += t
+    u >>= 16
+    return u.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
