@@ -163,6 +163,32 @@ int ltd_tree_accept(const float* logits, const int32_t* draft_tokens, const int3
                     void* stream);
 
 /*
+ * Greedy acceptance without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, results and validation as
+ * ltd_tree_accept, minus the workspace: the argmax partials go to a scratch
+ * array that the library holds on each GPU for the life of the process
+ * (ltd_tree_accept_noalloc_max_bytes() bytes, 4 MiB).  The call allocates
+ * nothing and frees nothing.
+ *
+ * Limits: ltd_tree_accept_workspace_size(B, Nmax, Voc) must not exceed
+ * ltd_tree_accept_noalloc_max_bytes() (B * Nmax * ceil(Voc / 8192) * 8 bytes;
+ * e.g. B = 16, Nmax = 256 and Voc = 262144 use 1 MiB), else LTD_EWORKSPACE and
+ * nothing is launched.  LTD_EHIP if the scratch's device address cannot be
+ * looked up on the current GPU.
+ * Every call on one GPU shares that GPU's scratch and keeps the last call's
+ * contents there (no call depends on them): calls that overlap on one GPU
+ * (different streams without ordering between them) race and give undefined
+ * results.
+ */
+size_t ltd_tree_accept_noalloc_max_bytes(void);
+
+int ltd_tree_accept_noalloc(const float* logits, const int32_t* draft_tokens,
+                            const int32_t* parents, const int32_t* n_nodes, int B, int Nmax,
+                            int Voc, int32_t* pred, int32_t* accepted_nodes, int32_t* out_tokens,
+                            int32_t* n_accepted, int validate, int32_t* status, void* stream);
+
+/*
  * Acceptance at temperature T > 0 (the paper's T = 1 setting; its rule is
  * the baseline's, not printed in the paper): recursive rejection sampling
  * over each node's children, which must have been drawn without replacement

@@ -54,6 +54,8 @@ EXPORTED = (
     "ltd_draft_expand",
     "ltd_tree_accept_sampling_workspace_size",
     "ltd_tree_accept_sampling",
+    "ltd_tree_accept_noalloc_max_bytes",
+    "ltd_tree_accept_noalloc",
 )
 
 
@@ -84,6 +86,10 @@ def lib() -> ctypes.CDLL:
         L.ltd_tree_accept_workspace_size.restype = sz
         L.ltd_tree_accept.argtypes = [P] * 4 + [i32] * 3 + [P] * 5 + [sz, i32, P, P]
         L.ltd_tree_accept.restype = i32
+        L.ltd_tree_accept_noalloc_max_bytes.argtypes = []
+        L.ltd_tree_accept_noalloc_max_bytes.restype = sz
+        L.ltd_tree_accept_noalloc.argtypes = [P] * 4 + [i32] * 3 + [P] * 4 + [i32, P, P]
+        L.ltd_tree_accept_noalloc.restype = i32
         L.ltd_kv_compact.argtypes = [P] * 7 + [i32] * 8 + [i64, i32, i32, P, P]
         L.ltd_kv_compact.restype = i32
         L.ltd_tree_verify_attn_num_splits.argtypes = [i32] * 9
@@ -195,6 +201,21 @@ def tree_accept(logits, draft_tokens, parents, n_nodes, pred, accepted_nodes, ou
         _p(accepted_nodes), _p(out_tokens), _p(n_accepted), _p(workspace),
         workspace.numel() * workspace.element_size(), int(validate), _p(status), _stream(stream))
     _check("ltd_tree_accept", rc)
+
+
+def accept_noalloc_max_bytes() -> int:
+    return int(lib().ltd_tree_accept_noalloc_max_bytes())
+
+
+def tree_accept_noalloc(logits, draft_tokens, parents, n_nodes, pred, accepted_nodes, out_tokens,
+                        n_accepted, *, validate: bool = False, status=None, stream=None):
+    """Greedy acceptance without a workspace; see ``ltd_tree_accept_noalloc``."""
+    B, Nmax, Voc = logits.shape
+    rc = lib().ltd_tree_accept_noalloc(
+        _p(logits), _p(draft_tokens), _p(parents), _p(n_nodes), B, Nmax, Voc, _p(pred),
+        _p(accepted_nodes), _p(out_tokens), _p(n_accepted), int(validate), _p(status),
+        _stream(stream))
+    _check("ltd_tree_accept_noalloc", rc)
 
 
 def kv_compact(k_cache, v_cache, prefix_len, new_prefix_len, accepted_nodes, n_accepted, *,

@@ -20,6 +20,8 @@
 // chip a device-scope atomic round trip costs about as much as the whole scan,
 // and an agent-scope fence (an L2 write-back) in every argmax workgroup costs
 // several times the argmax.
+#include <mutex>
+
 #include "ltd_device.hpp"
 #include "ltd_launch.hpp"
 
@@ -221,7 +223,35 @@ __global__ void __launch_bounds__(kScanThreads) accept_scan_kernel(
   }
 }
 
+// Scratch of the allocation-free entry point: the argmax partial keys live in
+// a file-scope device array instead of a caller workspace.  Each GPU the
+// library runs on holds its own copy for the life of the process.  Host code
+// never uses the array's name as an address (on the host it only stands for
+// the symbol); the device address of each GPU's copy is looked up once, with
+// that GPU current, and kept per device.
+constexpr size_t kNoAllocScratchBytes = size_t{4} << 20;
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+
+// The device address of this GPU's scratch, or nullptr when it cannot be had.
+void* noalloc_scratch_ptr() {
+  static std::once_flag once[kMaxScratchDevices];
+  static void* ptr[kMaxScratchDevices];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) return nullptr;
+  std::call_once(once[dev], [dev] {
+    void* p = nullptr;
+    ptr[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) == hipSuccess ? p : nullptr;
+  });
+  return ptr[dev];
+}
+
 }  // namespace
+
+size_t accept_noalloc_scratch_bytes() { return kNoAllocScratchBytes; }
+
+void* accept_noalloc_scratch() { return noalloc_scratch_ptr(); }
 
 size_t accept_workspace_bytes(int B, int Nmax, int Voc) {
   const int chunks = (Voc + kChunk - 1) / kChunk;

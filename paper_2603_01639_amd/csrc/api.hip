@@ -128,6 +128,35 @@ int ltd_tree_accept(const float* logits, const int32_t* draft_tokens, const int3
   return LTD_OK;
 }
 
+size_t ltd_tree_accept_noalloc_max_bytes(void) { return ltd::accept_noalloc_scratch_bytes(); }
+
+int ltd_tree_accept_noalloc(const float* logits, const int32_t* draft_tokens,
+                            const int32_t* parents, const int32_t* n_nodes, int B, int Nmax,
+                            int Voc, int32_t* pred, int32_t* accepted_nodes, int32_t* out_tokens,
+                            int32_t* n_accepted, int validate, int32_t* status, void* stream) {
+  if (B < 0 || Nmax < 1 || Nmax > LTD_MAX_NODES || Voc < 1) return LTD_EINVAL;
+  if (validate && !status) return LTD_EINVAL;
+  if (B == 0) return LTD_OK;
+  if (!logits || !draft_tokens || !parents || !n_nodes || !pred || !accepted_nodes ||
+      !out_tokens || !n_accepted)
+    return LTD_EINVAL;
+  if (ltd::accept_workspace_bytes(B, Nmax, Voc) > ltd::accept_noalloc_scratch_bytes())
+    return LTD_EWORKSPACE;
+  void* scratch = ltd::accept_noalloc_scratch();
+  if (!scratch) return LTD_EHIP;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (validate) {
+    if (ltd::launch_validate_tree(nullptr, nullptr, parents, n_nodes, B, Nmax, 0, 1, 0, 0, false,
+                                  status, st) != hipSuccess)
+      return LTD_EHIP;
+  }
+  if (ltd::launch_accept(logits, draft_tokens, parents, n_nodes, B, Nmax, Voc, pred,
+                         accepted_nodes, out_tokens, n_accepted, scratch,
+                         validate ? status : nullptr, st) != hipSuccess)
+    return LTD_EHIP;
+  return LTD_OK;
+}
+
 int ltd_kv_compact(void* k_cache, void* v_cache, const int32_t* block_table,
                    const int32_t* prefix_len, int32_t* new_prefix_len,
                    const int32_t* accepted_nodes, const int32_t* n_accepted, int B, int Nmax,

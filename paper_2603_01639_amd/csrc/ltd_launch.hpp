@@ -42,6 +42,10 @@ hipError_t launch_attention(const AttnShape& s, const AttnPlan& plan, const void
 
 // accept.hip
 size_t accept_workspace_bytes(int B, int Nmax, int Voc);
+// The allocation-free acceptance: bytes of the per-device scratch array, and
+// its device address on the current GPU (nullptr if it cannot be looked up).
+size_t accept_noalloc_scratch_bytes();
+void* accept_noalloc_scratch();
 hipError_t launch_accept(const float* logits, const int32_t* draft_tokens, const int32_t* parents,
                          const int32_t* n_nodes, int B, int Nmax, int Voc, int32_t* pred,
                          int32_t* accepted_nodes, int32_t* out_tokens, int32_t* n_accepted,
