@@ -66,8 +66,11 @@ def test_config5_deterministic():
     U.log(f"[parity] determinism {b.label}")
     dev = U.upload(b)
     a1 = U.gpu_attention(b, dev)
-    a2 = U.gpu_attention(b, dev, fill=3.0)
-    np.testing.assert_array_equal(a1, a2)
+    a2 = U.gpu_attention(b, dev, fill=3.0)  # a different fill: every written row is rewritten
+    for s in range(b.B):
+        n = int(b.n_nodes[s])
+        np.testing.assert_array_equal(a1[s, :n], a2[s, :n])
+        assert (U.as_f64(a2[s, n:], b.dtype) == 3.0).all()
     r1 = U.gpu_accept(b, dev)
     r2 = U.gpu_accept(b, dev)
     for x, y in zip(r1, r2):
