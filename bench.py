@@ -486,7 +486,7 @@ def binding_roof(call, alg_bytes, alg_flops, us):
 
 # The kernel sources behind each call's counters (launch plan included).
 CALL_SOURCES = {
-    "tree_verify_attn": ("attn_mfma.hip", "attn_plan.hip", "ltd_device.hpp"),
+    "tree_verify_attn": ("attn_mfma.hip", "attn_plan.hip", "stream_plan.hpp", "ltd_device.hpp"),
     "tree_accept": ("accept.hip", "ltd_device.hpp"),
 }
 

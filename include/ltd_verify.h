@@ -121,9 +121,10 @@ extern "C" {
  *               attention); anything else is LTD_EINVAL.
  *   workspace   device scratch of at least ltd_tree_verify_attn_workspace_size()
  *               bytes for the same (B, Nmax, Hq, Hkv, d, max_prefix, dtype) (that
- *               size covers every cache layout; it is 0 when no sequence can
- *               need more than one KV split, and workspace may then be NULL);
- *               its contents need no initialisation and are garbage afterwards.
+ *               size covers every cache layout; it is 0 on the row-wise path,
+ *               and workspace may then be NULL); it holds the partial results
+ *               of units cut between workgroups, needs no initialisation and
+ *               is garbage afterwards.
  */
 size_t ltd_tree_verify_attn_workspace_size(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
                                            int dtype);
@@ -249,15 +250,15 @@ int ltd_kv_compact(void* k_cache, void* v_cache, const int32_t* block_table,
                    int64_t layer_stride_elems, int dtype, int validate, int32_t* status,
                    void* stream);
 
-/* Number of KV splits (workgroups along the keys per sequence, kv head and
- * row tile) the attention launch uses for a sequence with prefix length
- * `prefix` and `n_nodes` tree nodes in a contiguous cache.  The tree's keys
- * go with the last prefix range or form a split of their own; a single split
- * writes the output without a merge pass (introspection for tests and
- * benchmarks; -1 on bad args, including prefix > max_prefix or
- * n_nodes > Nmax). */
-int ltd_tree_verify_attn_num_splits(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
-                                    int dtype, int prefix, int n_nodes);
+/* Workgroups of the attention launch for a shape and cache layout
+ * (kv_rows = capacity or block size, paged != 0 for a block table).  A bf16,
+ * head_dim 128 call lays all its (sequence, kv head, row tile) units' key
+ * tiles end to end and gives each of that many workgroups an equal share; a
+ * unit cut between workgroups is merged by a second kernel.  0 when the call
+ * runs on the row-wise kernel instead (fp32 or head_dim 64), -1 on bad args.
+ * Introspection for tests and benchmarks. */
+int ltd_tree_verify_attn_grid(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix, int dtype,
+                              int kv_rows, int paged);
 
 /*
  * Candidate token selection (section 3.2, "Candidate Token Selection"): of a

@@ -45,7 +45,7 @@ EXPORTED = (
     "ltd_tree_accept_workspace_size",
     "ltd_tree_accept",
     "ltd_kv_compact",
-    "ltd_tree_verify_attn_num_splits",
+    "ltd_tree_verify_attn_grid",
     "ltd_version",
     "ltd_select_candidates",
     "ltd_policy_workspace_size",
@@ -92,8 +92,8 @@ def lib() -> ctypes.CDLL:
         L.ltd_tree_accept_noalloc.restype = i32
         L.ltd_kv_compact.argtypes = [P] * 7 + [i32] * 8 + [i64, i32, i32, P, P]
         L.ltd_kv_compact.restype = i32
-        L.ltd_tree_verify_attn_num_splits.argtypes = [i32] * 9
-        L.ltd_tree_verify_attn_num_splits.restype = i32
+        L.ltd_tree_verify_attn_grid.argtypes = [i32] * 9
+        L.ltd_tree_verify_attn_grid.restype = i32
         L.ltd_select_candidates.argtypes = [P] * 5 + [i32] * 3 + [P] * 5 + [i32, P, P]
         L.ltd_select_candidates.restype = i32
         L.ltd_policy_workspace_size.argtypes = [i32] * 3
@@ -149,9 +149,10 @@ def attn_workspace_size(B, Nmax, Hq, Hkv, d, max_prefix, dtype) -> int:
     return int(lib().ltd_tree_verify_attn_workspace_size(B, Nmax, Hq, Hkv, d, max_prefix, dtype))
 
 
-def attn_num_splits(B, Nmax, Hq, Hkv, d, max_prefix, dtype, prefix, n_nodes) -> int:
-    return int(lib().ltd_tree_verify_attn_num_splits(B, Nmax, Hq, Hkv, d, max_prefix, dtype, prefix,
-                                                     n_nodes))
+def attn_grid(B, Nmax, Hq, Hkv, d, max_prefix, dtype, kv_rows, paged=False) -> int:
+    """Workgroups of the attention launch; see ``ltd_tree_verify_attn_grid``."""
+    return int(lib().ltd_tree_verify_attn_grid(B, Nmax, Hq, Hkv, d, max_prefix, dtype, kv_rows,
+                                               int(bool(paged))))
 
 
 def accept_workspace_size(B, Nmax, Voc) -> int:

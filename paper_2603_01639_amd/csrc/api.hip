@@ -2,6 +2,7 @@
 // plans and kernel dispatch.  No allocation, no synchronisation.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <mutex>
 
@@ -52,19 +53,25 @@ const char* ltd_version(void) { return "ltd_verify 0.1 (gfx950)"; }
 size_t ltd_tree_verify_attn_workspace_size(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
                                            int dtype) {
   if (!attn_args_ok(B, Nmax, Hq, Hkv, d, max_prefix, dtype) || !attn_supported(d, dtype)) return 0;
-  // The layout with the most splits (paged, one row per block) bounds every
-  // layout's need.
-  const ltd::AttnShape s = make_shape(B, Nmax, Hq, Hkv, d, max_prefix, 1, 1, dtype);
-  return ltd::plan_attention(s, device_cu_count()).workspace_bytes;
+  // The largest need over the layouts: a contiguous cache, and a paged one
+  // with one-row blocks (the smallest blocks shorten the split plan's splits
+  // the most, and send a batch from the stream plan to the split plan).
+  const ltd::AttnShape contiguous =
+      make_shape(B, Nmax, Hq, Hkv, d, max_prefix, max_prefix + Nmax, 0, dtype);
+  const ltd::AttnShape tiny_blocks = make_shape(B, Nmax, Hq, Hkv, d, max_prefix, 1, 1, dtype);
+  const int cus = device_cu_count();
+  return std::max(ltd::plan_attention(contiguous, cus).workspace_bytes,
+                  ltd::plan_attention(tiny_blocks, cus).workspace_bytes);
 }
 
-int ltd_tree_verify_attn_num_splits(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix,
-                                    int dtype, int prefix, int n_nodes) {
+int ltd_tree_verify_attn_grid(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix, int dtype,
+                              int kv_rows, int paged) {
   if (!attn_args_ok(B, Nmax, Hq, Hkv, d, max_prefix, dtype) || !attn_supported(d, dtype) ||
-      prefix < 0 || prefix > max_prefix || n_nodes < 0 || n_nodes > Nmax)
+      kv_rows < 1)
     return -1;
-  const ltd::AttnShape s = make_shape(B, Nmax, Hq, Hkv, d, max_prefix, 1, 0, dtype);
-  return ltd::attention_splits(ltd::plan_attention(s, device_cu_count()), prefix, n_nodes);
+  const ltd::AttnShape s =
+      make_shape(B, Nmax, Hq, Hkv, d, max_prefix, kv_rows, paged ? 1 : 0, dtype);
+  return ltd::attention_grid(ltd::plan_attention(s, device_cu_count()));
 }
 
 int ltd_tree_verify_attn(const void* q, const void* k_cache, const void* v_cache,

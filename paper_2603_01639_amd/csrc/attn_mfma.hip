@@ -10,12 +10,14 @@
 //   S^T[key][row] = K[key][:] . Q[row][:]        (v_mfma_f32_32x32x16_bf16)
 //   O^T[dim][row] += V^T[dim][key] . P^T[key][row]
 //
-// Work split: grid = (b*Hkv + g, row tile, KV split).  A workgroup of 8
-// wavefronts owns 8*32 stacked rows (32 per wave) and one KV split: a range of
-// prefix keys, and for the last split of a (sequence, kv head) also the
-// tree's own N keys under the ancestor mask.  With several splits each one
-// writes a partial result (its max, sum and normalised output) that
-// attn_merge_kernel combines; a single split writes the output directly.
+// Work split: a unit is one (sequence, kv head, row tile of up to 8*32
+// stacked rows).  Its work is its prefix key tiles and then the tree's keys
+// under the ancestor mask.  All units of the call are laid end to end and the
+// grid's workgroups take equal shares of that sequence (stream_plan.hpp): a
+// workgroup of 8 wavefronts (32 rows each) runs through its share unit by
+// unit.  A unit it covers whole gets its final output written directly; a
+// unit cut between workgroups gets a partial result (max, sum and normalised
+// output) from each of them, which attn_merge_kernel combines.
 //
 // K/V stream: 64-key tiles move from HBM straight into an LDS ring of
 // kStages slots with global_load_lds_dwordx4 (no register staging); a lane
@@ -40,6 +42,7 @@
 
 #include "ltd_device.hpp"
 #include "ltd_launch.hpp"
+#include "stream_plan.hpp"
 
 namespace ltd {
 namespace {
@@ -70,16 +73,13 @@ constexpr int kKLoads = kLoadsPerTile / 2;  // K (and V) chunks per lane per til
 // probabilities stay below 2^kLazyMax, exact in fp32 and well inside bf16
 // range, and the O/l rescale runs only when the max really moves.
 constexpr float kLazyMax = 8.f;
-constexpr int kMaxMergeSplits = 1024;          // the merge kernel's weight table (16 KiB)
-#ifndef LTD_WGS_PER_CU
-#define LTD_WGS_PER_CU 1
-#endif
-#ifndef LTD_STAGES
-#define LTD_STAGES 4
-#endif
-constexpr int kWgsPerCu = LTD_WGS_PER_CU;  // resident workgroups the split plan aims for
-constexpr int kStages = LTD_STAGES;        // K/V tiles in the LDS ring
-constexpr int kTileRows = kWaves * 32;       // stacked query rows per workgroup
+constexpr int kStages = 4;                // K/V tiles in the LDS ring
+constexpr int kMaxSplitTiles = 32;        // split plan: longest split in key tiles
+constexpr int kMaxMergeSplits = 1024;     // split plan: splits the merge takes at most
+constexpr int kTileRows = kWaves * 32;    // stacked query rows per workgroup (one unit)
+static_assert(kTileRows == plan::kUnitRows && kKT == plan::kKeyTile, "unit shape");
+
+struct MergeDesc;
 
 struct MfmaArgs {
   const uint16_t* q;
@@ -89,12 +89,17 @@ struct MfmaArgs {
   const int32_t* prefix_len;
   const int32_t* parents;
   const int32_t* n_nodes;
-  uint16_t* ws_o;  // [B*Hkv][max_splits][Mpad][128] bf16: the split's O / l
-  float* ws_ml;    // [B*Hkv][max_splits][Mpad][2]: max (log2 units), sum l
+  uint16_t* ws_o;  // [2W][256][128] bf16: a piece's O / l (slot 2s or 2s + 1)
+  float* ws_ml;    // [2W][256][2]: max (log2 units), sum l
+  MergeDesc* ws_desc;  // [units]: each unit's merge (after a 64-byte header: the unit count)
+  int max_units;       // units the launch can have at most (table entries)
   uint16_t* out;
   const int32_t* status;
-  int Nmax, Hq, Hkv, G, kv_rows, max_blocks;
-  int Mpad, split_keys, max_splits, tree_alone;
+  int B, Nmax, Hq, Hkv, G, kv_rows, max_blocks, max_prefix;
+  int W;  // stream plan: workgroups of the grid (a power of two)
+  // split plan: prefix keys per split, splits of the longest sequence, whether
+  // the tree may take a split of its own, row tiles per (sequence, kv head)
+  int split_keys, max_splits, tree_alone, row_tiles;
   float scale_log2;
   float lazy_gap;  // kLazyMax / scale_log2: the raw-score margin of the lazy max
 };
@@ -187,17 +192,20 @@ __device__ __forceinline__ void dma4(uint32_t lds, const void* lane_ptr) {
 // would also wait for every outstanding direct load).
 __device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
 
-constexpr int kMaxSplitBlocks = 1024;  // paged block ids one split may span
-#ifndef LTD_MAX_SPLIT_TILES
-#define LTD_MAX_SPLIT_TILES 32
-#endif
-// Longest split in key tiles: keeps any one workgroup's chain of tiles short
-// next to the whole grid's work when sequences of different lengths are
-// batched (a longer split would leave its compute unit the last one busy).
-constexpr int kMaxSplitTiles = LTD_MAX_SPLIT_TILES;
+constexpr int kMaxSplitBlocks = 3072;  // paged block ids one unit's share may span
+
+// One share of a workgroup's work (a unit's key range), planned by wave 0 and
+// read by every wave before it runs the share.
+struct ShareDesc {
+  int32_t b, g, rt, P, n, key_begin, n_pre, tree, whole, slot;
+};
+constexpr int kMaxShares = 16;  // shares planned per round
 
 struct Smem {
   unsigned char kv[kStages][kTileBytes];
+  ShareDesc share[kMaxShares];
+  int64_t next_pos;  // where the next planning round resumes
+  int32_t n_share, first;
   uint32_t anc[LTD_MAX_NODES][kAncWords];
   int16_t jump[LTD_MAX_NODES];     // jump pointers of the mask build
   int32_t par[LTD_MAX_NODES];      // the tree's parent links (mask build)
@@ -230,21 +238,25 @@ __device__ __forceinline__ LoadPlan make_load_plan(int wave, int lane) {
   return lp;
 }
 
-// The attention of one workgroup over one KV split: the prefix keys
-// [key_begin, key_begin + n_pre) and, for the last split of a (sequence, kv
-// head) (kTree), also the tree's keys [P, P + n) under the ancestor mask.
-// Tiles t < tA cover the first range, the rest the second; a tile never spans
-// both.  With a single split the workgroup writes the final output.
+// The attention of one workgroup over its share of one unit: the prefix keys
+// [key_begin, key_begin + n_pre) and, with kTree, also the tree's keys
+// [P, P + n) under the ancestor mask.  Tiles t < tA cover the first range, the
+// rest the second; a tile never spans both.  With final_out the share is the
+// whole unit and the normalised output goes to `out`; otherwise the share's
+// partial result goes to workspace slot `slot`.
 template <bool kTree>
-__device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g, int bg, int split,
-                                       int n_splits, int row0, int valid_rows, int key_begin,
-                                       int n_pre, int P) {
-  const int tid = threadIdx.x;
+__device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g, int row0,
+                                       int valid_rows, int key_begin, int n_pre, int P, int n,
+                                       bool final_out, int slot) {
+  // (an opaque copy of the thread index: a workgroup runs this once per share,
+  // and without it the compiler hoists every per-lane address out of the share
+  // loop and keeps it live, and spilled, across all of them)
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
   const int wave = tid / kWave;
   const int lane = tid % kWave;
   const int h = lane >> 5;
   const int l32 = lane & 31;
-  const int n = a.n_nodes[b];
   const int n_tree = kTree ? n : 0;  // keys of the second range
   const int tA = (n_pre + kKT - 1) / kKT;
   const int n_tiles = tA + (n_tree + kKT - 1) / kKT;
@@ -625,19 +637,17 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     accumulate(n_tiles - 1, pfa);
   }
 
-  // ---- results.  With one split the normalised output O / l goes straight
-  // to `out`.  Otherwise the split's partial result: (max in log2 units, sum)
+  // ---- results.  For a whole unit the normalised output O / l goes straight
+  // to `out`.  Otherwise the share's partial result: (max in log2 units, sum)
   // in fp32 and O / l in bf16 (half the bytes of raw fp32 partials; the merge
-  // weights each split by 2^(m - M) * l).  The O rows pass through LDS so that
-  // every store writes whole 256-byte rows (a wave's 32 partial rows are one
-  // contiguous 8 KiB block of the workspace).  Partials are stored
-  // non-temporally: the merge kernel reads them from another XCD, so keeping
-  // them dirty in this XCD's L2 only lengthens the write-back at the end of
-  // the kernel.
+  // weights each piece by 2^(m - M) * l), at the unit's row r in slot `slot`.
+  // The O rows pass through LDS so that every store writes whole 256-byte rows
+  // (a wave's 32 partial rows are one contiguous 8 KiB block of the
+  // workspace).  Partials are stored non-temporally: keeping them dirty in
+  // this XCD's L2 only lengthens the write-back at the end of the kernel.
   constexpr int kRowPitch = kD * 2 + 16;  // padded LDS row (bank spread)
   static_assert(kWaves * 32 * kRowPitch <= kStages * kTileBytes, "staging fits the ring");
-  const bool final_out = n_splits == 1;
-  const int64_t part = (static_cast<int64_t>(bg) * a.max_splits + split) * a.Mpad;
+  const int64_t part = static_cast<int64_t>(slot) * kTileRows - row0;  // + absolute row
   barrier_only();  // every wave is done with the K/V ring; reuse it for staging
   if (!active) return;
   unsigned char* stage = &sm.kv[0][0] + wave * (32 * kRowPitch);  // spans ring slots
@@ -697,12 +707,169 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   }
 }
 
-__global__ void __launch_bounds__(kThreads, 1) attn_mfma_kernel(MfmaArgs a) {
+// ---- the call's work axis (stream_plan.hpp), computed by each wave on its
+// own: lane l holds sequence c * 64 + l of chunk c.  Prefix lengths and node
+// counts are clamped into the range the launch was sized for, so malformed
+// data without validation cannot move any position off the planned axis.
+
+__device__ __forceinline__ plan::SeqCost lane_cost(const MfmaArgs& a, int b, int* P, int* n) {
+  *P = 0;
+  *n = 1;
+  if (b < a.B) {
+    *P = min(max(a.prefix_len[b], 0), a.max_prefix);
+    *n = min(max(a.n_nodes[b], 1), a.Nmax);
+  }
+  return plan::seq_cost(*P, *n, a.G);
+}
+
+__device__ __forceinline__ int64_t shfl_up_i64(int64_t v, int d) {
+  const int lo = __shfl_up(static_cast<int>(v), d, kWave);
+  const int hi = __shfl_up(static_cast<int>(v >> 32), d, kWave);
+  return (static_cast<int64_t>(hi) << 32) | static_cast<uint32_t>(lo);
+}
+__device__ __forceinline__ int64_t readlane_i64(int64_t v, int l) {
+  const int lo = __builtin_amdgcn_readlane(static_cast<int>(v), l);
+  const int hi = __builtin_amdgcn_readlane(static_cast<int>(v >> 32), l);
+  return (static_cast<int64_t>(hi) << 32) | static_cast<uint32_t>(lo);
+}
+
+// The call's sequence table on the axis, one sequence per lane: lane l of a
+// wave holds sequence l (its clamped prefix length and node count, first axis
+// position and axis length), and every lane holds the total length C.  With
+// more than 64 sequences the lanes hold the first 64 and positions past them
+// are found by rescanning the table (axis_find).
+struct Axis {
+  int P, n;
+  int64_t start, len;
+  int ubase;  // index of this lane's sequence's first unit
+  int64_t C;
+  int units;  // units of the whole call
+};
+
+// Inclusive prefix sum over the wave.
+__device__ __forceinline__ int64_t wave_scan_i64(int64_t x) {
+  const int lane = __lane_id();
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int64_t y = shfl_up_i64(x, d);
+    if (lane >= d) x += y;
+  }
+  return x;
+}
+
+__device__ Axis axis_load(const MfmaArgs& a) {
+  const int lane = __lane_id();
+  Axis ax{};
+  if (a.B == 1) {
+    // one sequence: scalar loads (a short round trip) and no scans
+    const int P = min(max(a.prefix_len[0], 0), a.max_prefix);
+    const int n = min(max(a.n_nodes[0], 1), a.Nmax);
+    const plan::SeqCost c = plan::seq_cost(P, n, a.G);
+    ax.P = P;
+    ax.n = n;
+    ax.start = 0;
+    ax.ubase = 0;
+    ax.len = lane == 0 ? a.Hkv * c.per_head : 0;
+    ax.C = a.Hkv * c.per_head;
+    ax.units = a.Hkv * c.rt;
+    return ax;
+  }
+  int64_t base = 0;
+  int ubase = 0;
+  for (int c0 = 0; c0 < a.B; c0 += kWave) {
+    int P, n;
+    const plan::SeqCost c = lane_cost(a, c0 + lane, &P, &n);
+    const int64_t len = c0 + lane < a.B ? a.Hkv * c.per_head : 0;
+    const int64_t x = wave_scan_i64(len);
+    const int nu = c0 + lane < a.B ? a.Hkv * c.rt : 0;
+    const int xu = static_cast<int>(wave_scan_i64(nu));
+    if (c0 == 0) {
+      ax.P = P;
+      ax.n = n;
+      ax.start = x - len;
+      ax.len = len;
+      ax.ubase = xu - nu;
+    }
+    base += readlane_i64(x, kWave - 1);
+    ubase += __builtin_amdgcn_readlane(xu, kWave - 1);
+  }
+  ax.C = base;
+  ax.units = ubase;
+  return ax;
+}
+
+// The sequence whose units hold axis position p (0 <= p < C).
+__device__ plan::SeqAt axis_find(const MfmaArgs& a, const Axis& ax, int64_t p) {
+  plan::SeqAt r{};
+  const uint64_t hit = __ballot(ax.len > 0 && ax.start <= p && p < ax.start + ax.len);
+  if (hit != 0) {
+    const int l = __ffsll(static_cast<long long>(hit)) - 1;
+    r.b = l;
+    r.P = __builtin_amdgcn_readlane(ax.P, l);
+    r.n = __builtin_amdgcn_readlane(ax.n, l);
+    r.pre = readlane_i64(ax.start, l);
+    r.ubase = __builtin_amdgcn_readlane(ax.ubase, l);
+    r.c = plan::seq_cost(r.P, r.n, a.G);
+    return r;
+  }
+  // past the first 64 sequences: rescan the table from the second chunk on
+  const int lane = __lane_id();
+  int64_t base = readlane_i64(ax.start + ax.len, kWave - 1);
+  int ubase = __builtin_amdgcn_readlane(ax.ubase, kWave - 1) +
+              __builtin_amdgcn_readlane(a.Hkv * plan::seq_cost(ax.P, ax.n, a.G).rt, kWave - 1);
+  for (int c0 = kWave; c0 < a.B; c0 += kWave) {
+    int P, n;
+    const plan::SeqCost c = lane_cost(a, c0 + lane, &P, &n);
+    const int64_t len = c0 + lane < a.B ? a.Hkv * c.per_head : 0;
+    const int64_t x = wave_scan_i64(len);
+    const int nu = c0 + lane < a.B ? a.Hkv * c.rt : 0;
+    const int xu = static_cast<int>(wave_scan_i64(nu));
+    const int64_t start = base + x - len;
+    const uint64_t h = __ballot(len > 0 && start <= p && p < start + len);
+    if (h != 0) {
+      const int l = __ffsll(static_cast<long long>(h)) - 1;
+      r.b = c0 + l;
+      r.P = __builtin_amdgcn_readlane(P, l);
+      r.n = __builtin_amdgcn_readlane(n, l);
+      r.pre = readlane_i64(start, l);
+      r.ubase = ubase + __builtin_amdgcn_readlane(xu - nu, l);
+      r.c = plan::seq_cost(r.P, r.n, a.G);
+      return r;
+    }
+    base += readlane_i64(x, kWave - 1);
+    ubase += __builtin_amdgcn_readlane(xu, kWave - 1);
+  }
+  return r;  // not reached for p < C
+}
+
+// What the merge kernel needs of a unit: whether it was cut and, if so, its
+// pieces (plan::MergeJob), written by the attention workgroup that owns the
+// unit's tree block so that the merge workgroups do not redo the partition's
+// arithmetic.  Entry i of the table is the call's unit i; the table's header
+// holds the call's unit count (entries past it are left from other calls).
+struct MergeDesc {
+  int32_t active, b, g, rt, n, sa, sa_first, t_pre;
+  int64_t U, C;
+  int32_t w, pad[3];
+};
+static_assert(sizeof(MergeDesc) == 64, "descriptor layout");
+
+// Workgroup w of the grid takes stream index s: the workgroups on one XCD
+// (w mod 8; the hardware deals workgroups to the 8 XCDs round robin) take one
+// contiguous eighth of the axis, in launch order, so the row tiles of one
+// (sequence, kv head), which read the same keys, run side by side on one L2.
+__device__ __forceinline__ int stream_index(int w, int W) { return (w % 8) * (W / 8) + w / 8; }
+
+// ---- split plan (one sequence): grid = (b * Hkv + g, row tile, KV split).
+// Each (sequence, kv head, row tile) unit is cut into KV splits of
+// split_keys prefix keys; the tree's keys join the last split or take one of
+// their own.  (sequence, kv head) is the fastest grid dimension: workgroups
+// are dealt to the 8 XCDs by linear id modulo 8, so each kv head's splits
+// share one XCD (its L2 holds their common Q rows and K/V).  A unit with one
+// split writes its output directly; otherwise split sp leaves its partial in
+// slot (bg * max_splits + sp) * row_tiles + row tile.
+__global__ void __launch_bounds__(kThreads, 1) attn_split_kernel(MfmaArgs a) {
   __shared__ __attribute__((aligned(16))) Smem sm;
-  // (sequence, kv head) is the fastest grid dimension: workgroups are dealt
-  // to the 8 XCDs by linear id modulo 8, so each kv head's splits and row
-  // tiles share one XCD (its L2 holds their common Q rows and K/V), and the
-  // XCDs receive equal shares of every split index.
   const int bg = blockIdx.x;
   const int rtile = blockIdx.y;
   const int split = blockIdx.z;
@@ -720,13 +887,14 @@ __global__ void __launch_bounds__(kThreads, 1) attn_mfma_kernel(MfmaArgs a) {
   // starts at P with none.
   const int key_begin = min(split * a.split_keys, P);
   const int n_pre = min(a.split_keys, P - key_begin);
+  const int slot = (bg * a.max_splits + split) * a.row_tiles + rtile;
   if (split == nsp - 1)
-    attend<true>(a, sm, b, g, bg, split, nsp, row0, valid_rows, key_begin, n_pre, P);
+    attend<true>(a, sm, b, g, row0, valid_rows, key_begin, n_pre, P, n, nsp == 1, slot);
   else
-    attend<false>(a, sm, b, g, bg, split, nsp, row0, valid_rows, key_begin, n_pre, P);
+    attend<false>(a, sm, b, g, row0, valid_rows, key_begin, n_pre, P, n, nsp == 1, slot);
 }
 
-// One wave per stacked row: combine the splits' partials
+// Split plan merge, one wave per stacked row: combine the splits' partials
 //   out = sum_s w_s * Ohat_s / sum_s w_s,  w_s = 2^(m_s - M) * l_s,  M = max_s m_s,
 // where Ohat_s = O_s / l_s is the split's normalised output (bf16).  Lane s
 // takes split s's (m, l); the 4 groups of 16 lanes each read one split's row
@@ -736,7 +904,7 @@ __global__ void __launch_bounds__(kThreads, 1) attn_mfma_kernel(MfmaArgs a) {
 // requested before the sequence's prefix length and node count arrive: every
 // row of the grid is inside the workspace's Mpad rows, and every split index
 // below max_splits inside its splits.
-__global__ void __launch_bounds__(256) attn_merge_kernel(MfmaArgs a) {
+__global__ void __launch_bounds__(256) attn_split_merge_kernel(MfmaArgs a) {
   __shared__ float w_s[4][kMaxMergeSplits];
   constexpr int kFirst = 16;  // splits whose rows are requested up front
   const int bg = blockIdx.x;
@@ -747,11 +915,12 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(MfmaArgs a) {
   const int row = blockIdx.y * 4 + wv;
   const int lane = threadIdx.x % kWave;
   const int grp = lane >> 4, col = lane & 15;  // split offset, 8-dim chunk
-  const int64_t part0 = static_cast<int64_t>(bg) * a.max_splits * a.Mpad + row;
+  const int Mpad = a.row_tiles * kTileRows;  // rows of a (sequence, kv head) unit set
+  const int64_t part0 = static_cast<int64_t>(bg) * a.max_splits * Mpad + row;
   const unsigned char* op = reinterpret_cast<const unsigned char*>(a.ws_o + part0 * kD) + col * 16;
-  const int64_t stride = static_cast<int64_t>(a.Mpad) * kD * 2;  // bytes between splits
+  const int64_t stride = static_cast<int64_t>(Mpad) * kD * 2;  // bytes between splits
   f32x2 ml0 = {-INFINITY, 0.f};
-  if (lane < a.max_splits) ml0 = *reinterpret_cast<const f32x2*>(a.ws_ml + (part0 + lane * a.Mpad) * 2);
+  if (lane < a.max_splits) ml0 = *reinterpret_cast<const f32x2*>(a.ws_ml + (part0 + lane * Mpad) * 2);
   u32x4 o0[kFirst / 4];
 #pragma unroll
   for (int u = 0; u < kFirst / 4; ++u) {
@@ -767,11 +936,11 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(MfmaArgs a) {
   const int n_splits = min(n_splits_of(P, n, a.split_keys, a.tree_alone), a.max_splits);
   if (n_splits == 1) return;  // the attention kernel wrote this row's output
   float M = lane < n_splits ? ml0.x : -INFINITY;
-  for (int s = lane + kWave; s < n_splits; s += kWave) M = fmaxf(M, a.ws_ml[(part0 + s * a.Mpad) * 2]);
+  for (int s = lane + kWave; s < n_splits; s += kWave) M = fmaxf(M, a.ws_ml[(part0 + s * Mpad) * 2]);
   M = wave_max(M);
   float wsum = 0.f;
   for (int s = lane; s < n_splits; s += kWave) {
-    const f32x2 ml = s == lane ? ml0 : *reinterpret_cast<const f32x2*>(a.ws_ml + (part0 + s * a.Mpad) * 2);
+    const f32x2 ml = s == lane ? ml0 : *reinterpret_cast<const f32x2*>(a.ws_ml + (part0 + s * Mpad) * 2);
     const float w = exp2_fast(ml.x - M) * ml.y;
     w_s[wv][s] = w;
     wsum += w;
@@ -828,7 +997,223 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(MfmaArgs a) {
   }
 }
 
+
+// ---- stream plan (batches): the workgroup's shares are planned in rounds of up to kMaxShares by wave 0
+// into LDS, then run one by one by the whole workgroup: the partition's state
+// (the sequence table, positions) is dead while the tile loop runs, which
+// keeps it out of the loop's registers.
+__global__ void __launch_bounds__(kThreads, 1) attn_stream_kernel(MfmaArgs a) {
+  __shared__ __attribute__((aligned(16))) Smem sm;
+  if (halted(a.status)) return;
+  const int s = stream_index(blockIdx.x, a.W);
+  const int wave = threadIdx.x / kWave;
+  bool started = false;
+  for (int round = 0;; ++round) {
+    if (wave == 0) {
+      const Axis ax = axis_load(a);
+      auto find = [&](int64_t p) { return axis_find(a, ax, p); };
+      const plan::Grid gr = plan::make_grid(ax.C, a.W);
+      if (blockIdx.x == 0 && round == 0 && threadIdx.x == 0)
+        *reinterpret_cast<int32_t*>(a.ws_desc) = ax.units;  // the merge table's header
+      bool first = round == 0 ? true : sm.first != 0;
+      const int64_t pos = round == 0 ? plan::range_lo(gr, s) : sm.next_pos;
+      int k = 0;
+      const int64_t next = plan::walk_shares(
+          s, gr, pos, first, kMaxShares, find,
+          [&](const plan::SeqAt& q, const plan::Unit& u, int64_t U, const plan::Share& sh,
+              bool whole, int slot) {
+            const plan::KeyRange keys = plan::share_keys(sh, q.P);
+            if (threadIdx.x == 0)
+              sm.share[k] = ShareDesc{q.b, u.g, u.rt, q.P, q.n, keys.begin, keys.count,
+                                      sh.tree ? 1 : 0, whole ? 1 : 0, slot};
+            ++k;
+            if (sh.tree) {  // this workgroup owns the unit's last item: its merge entry
+              const plan::MergeJob job = plan::unit_job(q, u, U, s, gr, find);
+              if (threadIdx.x == 0) {
+                MergeDesc d{};
+                d.active = job.active;
+                d.b = q.b;
+                d.g = u.g;
+                d.rt = u.rt;
+                d.n = q.n;
+                d.sa = job.sa;
+                d.sa_first = job.sa_first;
+                d.t_pre = q.c.t_pre;
+                d.U = U;
+                d.C = ax.C;
+                d.w = u.w;
+                a.ws_desc[1 + plan::unit_index(q, u)] = d;
+              }
+            }
+          });
+      if (threadIdx.x == 0) {
+        sm.n_share = k;
+        sm.first = first ? 1 : 0;
+        sm.next_pos = next < plan::range_lo(gr, s + 1) ? next : -1;
+      }
+    }
+    __syncthreads();
+    const int n_share = sm.n_share;
+    const int64_t next_pos = sm.next_pos;
+    for (int i = 0; i < n_share; ++i) {
+      if (started) __syncthreads();  // the last share's staging is done with the ring
+      started = true;
+      const ShareDesc d = sm.share[i];
+      const int row0 = d.rt * kTileRows;
+      if (d.tree)
+        attend<true>(a, sm, d.b, d.g, row0, a.G * d.n, d.key_begin, d.n_pre, d.P, d.n,
+                     d.whole != 0, d.slot);
+      else
+        attend<false>(a, sm, d.b, d.g, row0, a.G * d.n, d.key_begin, d.n_pre, d.P, d.n,
+                      d.whole != 0, d.slot);
+    }
+    if (next_pos < 0) break;
+    __syncthreads();  // every wave has read this round's shares
+  }
+}
+
+// Merge of a unit cut between workgroups: out = sum_p w_p * Ohat_p / sum_p w_p,
+// w_p = 2^(m_p - M) * l_p, M = max_p m_p, over the unit's pieces p in
+// workgroup order, where Ohat_p = O_p / l_p is the piece's normalised output
+// (bf16).  blockIdx.x = the unit (its entry in the merge table says whether it
+// was cut), blockIdx.y picks 16 of its rows: each wave takes 4 rows, 16 lanes
+// per row and 16 bytes (8 dims) per lane.  Lane k of a wave works out the
+// slot of piece k once (64 pieces per round); every lane then walks the
+// pieces in batches of 8 with all their loads in flight, keeping a running
+// max (each batch rescales the sums at most once), so a unit of up to 8
+// pieces takes a single round of loads.
+__global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
+  constexpr int kBatch = 8;
+  if (halted(a.status)) return;
+  const int units = *reinterpret_cast<const int32_t*>(a.ws_desc);
+  const MergeDesc d = a.ws_desc[1 + blockIdx.x];
+  if (static_cast<int>(blockIdx.x) >= units || !d.active) return;
+  const int wv = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  const int rows = min(a.G * d.n - d.rt * kTileRows, kTileRows);
+  const int r0 = blockIdx.y * 16 + wv * 4;
+  if (r0 >= rows) return;
+  const int r = min(r0 + (lane >> 4), rows - 1);  // (rows past the unit's compute its last, unstored)
+  const int col = lane & 15;
+  plan::MergeJob job{};
+  job.active = true;
+  job.sa = d.sa;
+  job.sa_first = d.sa_first != 0;
+  job.U = d.U;
+  job.u.w = d.w;
+  job.q.c.t_pre = d.t_pre;
+  const plan::Grid gr = plan::make_grid(d.C, a.W);
+  const int npieces = d.active ? plan::owner(gr, d.U + static_cast<int64_t>(d.w) * d.t_pre) - d.sa + 1 : 0;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float wsum = 0.f;
+  float M = -INFINITY;  // running max: acc and wsum are relative to 2^M
+  for (int c0 = 0; c0 < npieces; c0 += kWave) {
+    const int cnt = min(kWave, npieces - c0);
+    const int my_slot = lane < cnt ? plan::merge_piece_slot(job, c0 + lane, gr) : -1;
+    for (int k0 = 0; k0 < cnt; k0 += kBatch) {
+      f32x2 ml[kBatch];
+      u32x4 o[kBatch];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int slot = k0 + j < cnt ? __builtin_amdgcn_readlane(my_slot, k0 + j) : -1;
+        ml[j] = (f32x2){-INFINITY, 0.f};
+        o[j] = (u32x4){0u, 0u, 0u, 0u};
+        if (slot >= 0) {
+          const int64_t row = static_cast<int64_t>(slot) * kTileRows + r;
+          ml[j] = *reinterpret_cast<const f32x2*>(a.ws_ml + row * 2);
+          o[j] = *reinterpret_cast<const u32x4*>(a.ws_o + row * kD + col * 8);
+        }
+      }
+      // the batch's pieces join the running sums (one rescale per batch)
+      float Mb = M;
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) Mb = fmaxf(Mb, ml[j].x);
+      if (Mb > M) {
+        const float alpha = M == -INFINITY ? 0.f : exp2_fast(M - Mb);
+        wsum *= alpha;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] *= alpha;
+        M = Mb;
+      }
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const float w = ml[j].y > 0.f ? exp2_fast(ml[j].x - M) * ml[j].y : 0.f;
+        wsum += w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[2 * e] += w * bf16_to_f32(static_cast<uint16_t>(o[j][e] & 0xFFFFu));
+          acc[2 * e + 1] += w * bf16_to_f32(static_cast<uint16_t>(o[j][e] >> 16));
+        }
+      }
+    }
+  }
+  if (r0 + (lane >> 4) >= rows) return;
+  const float inv = 1.f / wsum;
+  const int row = d.rt * kTileRows + r;  // stacked row = node * G + head in group
+  const int node = row / a.G;
+  const int hq = d.g * a.G + row % a.G;
+  uint16_t* orow = a.out + ((static_cast<int64_t>(d.b) * a.Nmax + node) * a.Hq + hq) * kD;
+  u32x4 v;
+  v.x = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+  v.y = pack_bf16x2(acc[2] * inv, acc[3] * inv);
+  v.z = pack_bf16x2(acc[4] * inv, acc[5] * inv);
+  v.w = pack_bf16x2(acc[6] * inv, acc[7] * inv);
+  *reinterpret_cast<u32x4*>(orow + col * 8) = v;
+}
+
 }  // namespace
+
+namespace {
+
+constexpr int kMinTilesPerWg = 2;   // a share shorter than this is mostly fixed cost
+constexpr int kMaxGrid = 1024;      // workgroups of the attention grid at most
+
+// Stacked-row tiles and key tiles of the longest unit the launch allows.
+int64_t max_unit_tiles(const AttnShape& s) {
+  return (s.max_prefix + kKT - 1) / kKT + (s.Nmax + kKT - 1) / kKT;
+}
+int64_t max_units(const AttnShape& s) {
+  const int64_t rows = static_cast<int64_t>(s.Hq / s.Hkv) * s.Nmax;
+  return static_cast<int64_t>(s.B) * s.Hkv * ((rows + kTileRows - 1) / kTileRows);
+}
+
+// Whether every workgroup's share of a grid of W fits the paged block table
+// staged in LDS: a share is at most one unit's keys and, on the axis, at most
+// (C / W) / 2 + 1 key tiles (the smallest tile weight is 2), plus the tree.
+bool share_fits(const AttnShape& s, int W) {
+  if (s.max_blocks <= 0) return true;  // contiguous cache: no table
+  const int64_t unit_rows = static_cast<int64_t>(s.max_prefix) + s.Nmax;
+  const int64_t axis_tiles = max_units(s) * max_unit_tiles(s) * plan::tile_weight(8);
+  const int64_t share_rows =
+      std::min(unit_rows, (axis_tiles / W / 2 + 2) * kKT + static_cast<int64_t>(s.Nmax));
+  return share_rows / s.kv_rows + 2 <= kMaxSplitBlocks;
+}
+
+// Stream plan grid: W workgroups, a power of two of at least 8 (one eighth of
+// the axis per XCD; the partition's arithmetic is then shifts),
+// at most one resident round (one workgroup per compute unit), each with at
+// least kMinTilesPerWg key tiles of the largest call the shape allows.  It
+// does not depend on the cache layout, so neither does the workspace.
+int choose_grid(const AttnShape& s, int num_cus) {
+  const int64_t tiles = max_units(s) * max_unit_tiles(s);
+  const int64_t want = std::min<int64_t>(std::min(num_cus, kMaxGrid), tiles / kMinTilesPerWg);
+  int W = 8;
+  while (2 * W <= want) W *= 2;
+  return W;
+}
+
+constexpr size_t kSlotBytes = static_cast<size_t>(kTileRows) * (kD * sizeof(uint16_t) + 2 * sizeof(float));
+constexpr size_t kDescBytes = 64;  // sizeof(MergeDesc)
+
+}  // namespace
+
+// Single sequences take the split plan (every unit has the same length, and
+// the plan's cost model picks the split length and whether the tree keys get
+// a split of their own); batches take the stream plan, which balances units
+// of different lengths, unless a paged layout's blocks are so small that a
+// workgroup's share could span more block ids than the LDS table holds (the
+// split plan shortens its splits for those).
+bool use_stream(const AttnShape& s) { return s.B > 1 && share_fits(s, choose_grid(s, 256)); }
 
 // Longest split (in keys, a multiple of the key tile) whose paged block ids
 // fit the LDS table: the last split's rows (its prefix keys plus up to Nmax
@@ -848,22 +1233,6 @@ int64_t worst_split_key_cap(const AttnShape& s) {
   w.kv_rows = 1;
   w.max_blocks = 1;
   return split_key_cap(w);
-}
-
-bool mfma_supported(const AttnShape& s) {
-  const int64_t cap = worst_split_key_cap(s);
-  return s.dtype == LTD_DTYPE_BF16 && s.d == kD && cap >= 2 * kKT &&
-         s.max_prefix <= cap * kMaxMergeSplits;
-}
-
-// Estimated time of one plan, in units of one key tile's time for a
-// workgroup: the rounds of resident workgroups times the longest split plus a
-// workgroup's fixed cost (loading Q, writing the result: about three tiles),
-// and the merge kernel when a sequence has several splits.  The sequence
-// priced is the longest the call allows (max_prefix keys, Nmax nodes).
-int attention_splits(const AttnPlan& p, int prefix, int n) {
-  if (!p.mfma) return 1;
-  return n_splits_of(prefix, n, p.split_keys, p.tree_alone ? 1 : 0);
 }
 
 static double plan_cost(int64_t P, int n, int64_t sk, bool alone, int64_t units, int64_t target) {
@@ -886,19 +1255,18 @@ static double plan_cost(int64_t P, int n, int64_t sk, bool alone, int64_t units,
          (S > 1 ? kMergeTiles + S / 32.0 : 0.0);
 }
 
-void plan_mfma(const AttnShape& s, int num_cus, AttnPlan* p) {
+void plan_split(const AttnShape& s, int num_cus, AttnPlan* p) {
   const int G = s.Hq / s.Hkv;
-  p->rows = G * s.Nmax;
-  p->tile_rows = kTileRows;
-  p->row_tiles = (p->rows + kTileRows - 1) / kTileRows;
+  const int rows = G * s.Nmax;
+  p->row_tiles = (rows + kTileRows - 1) / kTileRows;
   // A (sequence, kv head, row tile) unit is split along the keys into about
-  // as many workgroups as keep one resident round of kWgsPerCu workgroups per
+  // as many workgroups as keep one resident round of one workgroup per
   // compute unit busy (a second, nearly empty round would double the kernel
   // time).  That gives the shortest split considered; a split holds at least
   // two key tiles, at most the paged table's cap, and the merge kernel's
   // table bounds the number of splits.
   const int64_t units = static_cast<int64_t>(s.B) * s.Hkv * p->row_tiles;
-  const int64_t target = static_cast<int64_t>(kWgsPerCu) * num_cus;
+  const int64_t target = num_cus;
   const int64_t want = std::max<int64_t>(1, target / units);
   const int64_t mp = s.max_prefix;
   const int64_t cap = std::min(split_key_cap(s), static_cast<int64_t>(kMaxSplitTiles) * kKT);
@@ -939,6 +1307,35 @@ void plan_mfma(const AttnShape& s, int num_cus, AttnPlan* p) {
   p->workspace_bytes =
       bound > 1 ? static_cast<size_t>(slots) * (kD * sizeof(uint16_t) + 2 * sizeof(float)) : 0;
   p->mfma = true;
+  p->stream = false;
+  p->grid = s.B * s.Hkv * p->row_tiles * p->max_splits;
+}
+
+// The split plan needs splits of at least two key tiles whose block ids fit
+// the LDS table even with one-row blocks, and at most kMaxMergeSplits of them.
+bool mfma_supported(const AttnShape& s) {
+  if (s.dtype != LTD_DTYPE_BF16 || s.d != kD) return false;
+  if (use_stream(s)) return true;
+  const int64_t cap = worst_split_key_cap(s);
+  return cap >= 2 * kKT && s.max_prefix <= cap * kMaxMergeSplits;
+}
+
+int attention_grid(const AttnPlan& p) { return p.mfma ? p.grid : 0; }
+
+// Stream plan: two partial slots per workgroup and the merge table (a 64-byte
+// header and one entry per unit the call can have).
+void plan_stream(const AttnShape& s, int num_cus, AttnPlan* p) {
+  p->mfma = true;
+  p->stream = true;
+  p->grid = choose_grid(s, num_cus);
+  p->workspace_bytes = 2 * static_cast<size_t>(p->grid) * kSlotBytes + (1 + max_units(s)) * kDescBytes;
+}
+
+void plan_mfma(const AttnShape& s, int num_cus, AttnPlan* p) {
+  if (use_stream(s))
+    plan_stream(s, num_cus, p);
+  else
+    plan_split(s, num_cus, p);
 }
 
 hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q,
@@ -946,7 +1343,7 @@ hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q
                             const int32_t* prefix_len, const int32_t* parents,
                             const int32_t* n_nodes, void* out, float scale, void* workspace,
                             const int32_t* status, hipStream_t stream) {
-  MfmaArgs a;
+  MfmaArgs a{};
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k_cache);
   a.v = static_cast<const uint16_t*>(v_cache);
@@ -954,32 +1351,48 @@ hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q
   a.prefix_len = prefix_len;
   a.parents = parents;
   a.n_nodes = n_nodes;
-  const int64_t Mpad = static_cast<int64_t>(p.row_tiles) * kTileRows;
-  const int64_t slots = static_cast<int64_t>(s.B) * s.Hkv * p.max_splits * Mpad;
-  a.ws_o = static_cast<uint16_t*>(workspace);
-  a.ws_ml = reinterpret_cast<float*>(a.ws_o + slots * kD);
   a.out = static_cast<uint16_t*>(out);
   a.status = status;
+  a.B = s.B;
   a.Nmax = s.Nmax;
   a.Hq = s.Hq;
   a.Hkv = s.Hkv;
   a.G = s.Hq / s.Hkv;
   a.kv_rows = s.kv_rows;
   a.max_blocks = s.max_blocks;
-  a.Mpad = static_cast<int>(Mpad);
-  a.split_keys = p.split_keys;
-  a.max_splits = p.max_splits;
-  a.tree_alone = p.tree_alone ? 1 : 0;
+  a.max_prefix = s.max_prefix;
   a.scale_log2 = scale * kLog2e;
   a.lazy_gap = kLazyMax / a.scale_log2;
-  const dim3 grid(s.B * s.Hkv, p.row_tiles, p.max_splits);
-  hipLaunchKernelGGL(attn_mfma_kernel, grid, dim3(kThreads), 0, stream, a);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  a.ws_o = static_cast<uint16_t*>(workspace);
+  if (!p.stream) {
+    a.split_keys = p.split_keys;
+    a.max_splits = p.max_splits;
+    a.tree_alone = p.tree_alone ? 1 : 0;
+    a.row_tiles = p.row_tiles;
+    const size_t slots = static_cast<size_t>(s.B) * s.Hkv * p.max_splits * p.row_tiles * kTileRows;
+    a.ws_ml = reinterpret_cast<float*>(ws + slots * kD * 2);
+    const dim3 grid(s.B * s.Hkv, p.row_tiles, p.max_splits);
+    hipLaunchKernelGGL(attn_split_kernel, grid, dim3(kThreads), 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || p.max_splits == 1) return e;  // one split: the output is final
+    // (sequence, kv head) fastest, as for the attention grid: a head's merge
+    // runs on the XCD whose workgroups wrote its partials.
+    const dim3 mgrid(s.B * s.Hkv, static_cast<unsigned>((p.row_tiles * kTileRows + 3) / 4));
+    hipLaunchKernelGGL(attn_split_merge_kernel, mgrid, dim3(256), 0, stream, a);
+    return hipGetLastError();
+  }
+  const size_t slots = static_cast<size_t>(2) * p.grid * kTileRows;
+  a.ws_ml = reinterpret_cast<float*>(ws + slots * kD * 2);
+  a.ws_desc = reinterpret_cast<MergeDesc*>(ws + slots * (kD * 2 + 2 * sizeof(float)));
+  a.W = p.grid;
+  a.max_units = static_cast<int>(max_units(s));
+  hipLaunchKernelGGL(attn_stream_kernel, dim3(p.grid), dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || p.max_splits == 1) return e;  // one split: the output is final
-  // (sequence, kv head) fastest, as for the attention grid: a head's merge
-  // runs on the XCD whose workgroups wrote its partials.
-  const dim3 mgrid(s.B * s.Hkv, static_cast<unsigned>((Mpad + 3) / 4));
-  hipLaunchKernelGGL(attn_merge_kernel, mgrid, dim3(256), 0, stream, a);
+  if (e != hipSuccess) return e;
+  // One merge workgroup column per possible unit, 16 rows per workgroup.
+  hipLaunchKernelGGL(attn_stream_merge_kernel, dim3(a.max_units, kTileRows / 16), dim3(256), 0,
+                     stream, a);
   return hipGetLastError();
 }
 

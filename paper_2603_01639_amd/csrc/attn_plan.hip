@@ -24,11 +24,7 @@ AttnPlan plan_attention(const AttnShape& s, int num_cus) {
     plan_mfma(s, num_cus, &p);
     return p;
   }
-  p.rows = (s.Hq / s.Hkv) * s.Nmax;
-  p.row_tiles = 1;
-  p.tile_rows = p.rows;
-  p.split_keys = 0;
-  p.max_splits = 1;
+  p.grid = 0;
   p.mfma = false;
   p.workspace_bytes = 0;
   return p;

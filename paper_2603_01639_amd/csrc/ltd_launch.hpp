@@ -22,18 +22,18 @@ struct AttnShape {
   int B, Nmax, Hq, Hkv, d, max_prefix, kv_rows, max_blocks, dtype;
 };
 struct AttnPlan {
-  int rows;        // stacked query rows per (sequence, kv head) = G * Nmax
-  int row_tiles;   // workgroups along the stacked rows
-  int tile_rows;   // rows per workgroup
-  int split_keys;  // prefix keys per split (multiple of the key tile)
-  int max_splits;  // KV splits of the longest sequence (max_prefix keys, Nmax nodes)
-  bool tree_alone; // the tree's keys may take a split of their own
-  bool mfma;       // bf16 MFMA split-KV path (else the row-wise VALU path)
+  int grid;          // workgroups of the MFMA attention grid (0 on the row-wise path)
+  bool mfma;         // bf16 MFMA path (else the row-wise VALU path)
+  bool stream;       // stream plan (batches) rather than the split plan (one sequence)
+  int split_keys;    // split plan: prefix keys per split (a multiple of the key tile)
+  int max_splits;    // split plan: splits of the longest sequence
+  int row_tiles;     // split plan: row tiles per (sequence, kv head)
+  bool tree_alone;   // split plan: the tree's keys may take a split of their own
   size_t workspace_bytes;
 };
 AttnPlan plan_attention(const AttnShape& s, int num_cus);
-// KV splits of a sequence with `prefix` keys and `n` tree nodes under a plan.
-int attention_splits(const AttnPlan& p, int prefix, int n);
+// Workgroups the attention launch uses under a plan (0 on the row-wise path).
+int attention_grid(const AttnPlan& p);
 hipError_t launch_attention(const AttnShape& s, const AttnPlan& plan, const void* q,
                             const void* k_cache, const void* v_cache, const int32_t* block_table,
                             const int32_t* prefix_len, const int32_t* parents,

@@ -36,8 +36,8 @@ def test_version_and_workspace_queries():
     assert ltd.accept_workspace_size(1, 60, 128256) == 1 * 60 * 16 * 8
     assert ltd.accept_workspace_size(1, 300, 10) == 0  # Nmax above the node limit
     assert ltd.attn_workspace_size(1, 60, 32, 8, 96, 2048, ltd.DTYPE_BF16) == 0  # unsupported d
-    assert ltd.attn_num_splits(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 4096, 60) == -1
-    assert ltd.attn_num_splits(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 2048, 61) == -1
+    assert ltd.attn_grid(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 0) == -1  # kv_rows < 1
+    assert ltd.attn_grid(1, 300, 32, 8, 128, 2048, ltd.DTYPE_BF16, 4096) == -1  # Nmax > 256
 
 
 def test_library_links_only_hip_runtime():
@@ -64,28 +64,35 @@ def test_binding_signatures_match_header():
         assert len(getattr(lib, name).argtypes) == nparams, name
 
 
-def test_bf16_head128_workloads_plan_the_mfma_split_path():
-    """The 8B/32B-shaped bf16 shapes spread each (sequence, kv head) over
-    several KV splits (B=1 leaves most compute units idle otherwise).  The
-    16-sequence 70B-shaped batch already has more units than compute units;
-    its splits are only capped at 32 key tiles (2048 keys) so that no single
-    workgroup's chain of tiles dominates, and a sequence that fits one split
-    is written without a merge pass.  Where compute units are left over, the
-    tree's keys get a split of their own.  The workspace size covers the paged
-    layout with the most splits.  fp32 and d=64 run on the row-wise kernel."""
-    for B, Nmax, Hq, Hkv, P in ((1, 60, 32, 8, 2048), (1, 60, 32, 8, 16384), (1, 256, 64, 8, 4096)):
-        assert ltd.attn_num_splits(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16, P, Nmax) > 1
-        assert ltd.attn_workspace_size(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16) > 0
-    # 8B shape, prefix 2048: 16 two-tile prefix splits and the 60-node tree
-    # in a split of its own (the last prefix split has no room for it)
-    assert ltd.attn_num_splits(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 2048, 60) == 17
-    assert ltd.attn_num_splits(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 2048, 0) == 16
-    assert ltd.attn_num_splits(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 100, 60) == 1
-    assert ltd.attn_num_splits(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16, 8192, 128) == 4
-    assert ltd.attn_num_splits(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16, 2048, 128) == 1
-    assert ltd.attn_num_splits(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16, 0, 128) == 1
-    assert ltd.attn_workspace_size(16, 128, 64, 8, 128, 8192, ltd.DTYPE_BF16) > 0
-    assert ltd.attn_num_splits(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32, 128, 16) == 1
+def test_bf16_head128_workloads_plan_the_mfma_grid():
+    """bf16 head_dim 128 shapes run on the MFMA kernels.  A single sequence
+    takes the split plan: grid (kv heads, row tiles, KV splits), e.g. the
+    8B-shaped step at prefix 2048 cuts each kv head's prefix into 16 splits of
+    two key tiles and gives the 60-node tree a split of its own (8 x 17
+    workgroups).  A batch takes the stream plan: a power of two of at least 8
+    workgroups (one eighth of the work per XCD), at most one per compute unit,
+    two partial slots each.  fp32 and head_dim 64 run on the row-wise kernel
+    (grid 0, no workspace)."""
+    assert ltd.attn_grid(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 2108) == 8 * 17
+    for P, N, Hq in ((16384, 60, 32), (4096, 256, 64), (4096, 8, 64)):
+        g = ltd.attn_grid(1, N, Hq, 8, 128, P, ltd.DTYPE_BF16, P + N)
+        assert g > 8 and g % 8 == 0, (P, N, Hq, g)
+        assert ltd.attn_workspace_size(1, N, Hq, 8, 128, P, ltd.DTYPE_BF16) > 0
+    slot = 256 * (128 * 2 + 8)
+    for B, Nmax, Hq, Hkv, P, W in ((16, 128, 64, 8, 8192, 256), (2, 60, 32, 8, 2048, 256),
+                                   (2, 1, 8, 8, 0, 8)):
+        g = ltd.attn_grid(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16, P + Nmax)
+        assert g == W, (B, Nmax, Hq, Hkv, P, g)
+        assert g == ltd.attn_grid(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16, 16, paged=True)
+        assert ltd.attn_workspace_size(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16) >= 2 * g * slot
+    # blocks so small that a stream share could span more block ids than the
+    # LDS table holds: the split plan takes the batch (grid kv heads x row
+    # tiles x splits, not a power of two)
+    g = ltd.attn_grid(2, 64, 8, 8, 128, 400000, ltd.DTYPE_BF16, 1, paged=True)
+    assert g > 0 and g % 16 == 0 and g & (g - 1) != 0
+    assert ltd.attn_grid(2, 64, 8, 8, 128, 200000, ltd.DTYPE_BF16, 16, paged=True) == 256
+    assert ltd.attn_grid(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32, 144) == 0
+    assert ltd.attn_grid(1, 16, 8, 8, 64, 128, ltd.DTYPE_BF16, 144) == 0
     assert ltd.attn_workspace_size(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32) == 0
 
 

@@ -6,6 +6,7 @@ import pytest
 
 import gpu_util as U
 import paper_2603_01639_amd as ltd
+import partition_cases as PC
 import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -171,35 +172,18 @@ def test_argmax_ties_signed_zero_and_ragged_vocab():
 
 
 @pytest.mark.parametrize("block_size", [0, 16])
-@pytest.mark.parametrize("P,N,Hq", [(2048, 60, 32), (1999, 60, 32), (2048, 128, 8)])
-def test_tree_keys_in_a_split_of_their_own(P, N, Hq, block_size):
-    """A prefix spanning many short splits whose last one is (nearly) full:
-    the tree's keys take a split of their own (one or two tiles), and with
-    P=1999 the last prefix split ends in a partial tile."""
-    rng = np.random.default_rng(P + N)
-    b = _custom([W.tree_uniform_parent(rng, N)], [P], Hq=Hq, Hkv=8, Nmax=N, block_size=block_size,
-                seed=P + N, label=f"tree split P={P} N={N} block={block_size}")
-    shape = (b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix, b.dtype)
-    assert ltd.attn_num_splits(*shape, P, N) == ltd.attn_num_splits(*shape, P, 0) + 1 > 2
-    _full_step(b)
-
-
-@pytest.mark.parametrize("block_size", [0, 16])
-def test_single_split_batch_writes_output_directly(block_size):
-    """A batch whose longest prefix fits one KV split: every (sequence, kv
-    head) is one workgroup that also takes the tree keys and writes the output
-    itself (no workspace, no merge pass), with rows spread over several row
-    tiles and padded rows in the last one."""
-    rng = np.random.default_rng(41 + block_size)
-    sizes = (40, 1, 33, 64, 17, 5, 28, 60, 9, 50, 3, 64)
-    trees = [W.tree_uniform_parent(rng, n) for n in sizes]
-    prefix = [int(p) for p in rng.integers(0, 129, size=len(sizes))]
-    prefix[1], prefix[4] = 0, 128
-    b = _custom(trees, prefix, Hq=32, Hkv=4, Nmax=64, block_size=block_size, seed=41,
-                label=f"single-split batch block={block_size}")
-    assert ltd.attn_workspace_size(b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix, b.dtype) == 0
-    assert ltd.attn_num_splits(b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix, b.dtype, b.max_prefix,
-                               b.Nmax) == 1
+@pytest.mark.parametrize("case", PC.CASES, ids=[c.label for c in PC.CASES])
+def test_work_partition_cases(case, block_size):
+    """Batches whose work partition holds a share that is a tree block alone,
+    workgroups with nothing to do, units written whole and units cut into many
+    pieces (the host test of the partition checks that these batches cover
+    those cases), contiguous and paged."""
+    rng = np.random.default_rng(len(case.prefix) * 1000 + case.Nmax + block_size)
+    trees = [W.tree_uniform_parent(rng, n) for n in case.nodes]
+    b = _custom(trees, list(case.prefix), Hq=case.Hq, Hkv=case.Hkv, Nmax=case.Nmax,
+                block_size=block_size, seed=case.Nmax, label=f"{case.label} block={block_size}")
+    assert ltd.attn_grid(b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix, b.dtype, b.kv_rows,
+                         paged=b.paged) > 0
     _full_step(b)
 
 
@@ -240,3 +224,16 @@ def test_accept_workspace_reused_across_calls():
         torch.cuda.synchronize()
         U.check_accept(b, (pred.cpu().numpy(), acc.cpu().numpy(), toks.cpu().numpy(),
                            nacc.cpu().numpy()))
+
+
+def test_batch_of_one_row_blocks_takes_the_split_plan():
+    """A batch whose paged blocks are one row each: a stream share could span
+    more block ids than the LDS table holds, so the batch runs on the split
+    plan (its splits shortened to fit the table)."""
+    rng = np.random.default_rng(4242)
+    trees = [W.tree_uniform_parent(rng, n) for n in (37, 64)]
+    b = _custom(trees, [47000, 30000], Hq=24, Hkv=3, block_size=1, seed=4242,
+                label="one-row blocks B=2 P=47000")
+    g = ltd.attn_grid(b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix, b.dtype, b.kv_rows, paged=True)
+    assert g > 0 and g & (g - 1) != 0  # not the stream plan's power-of-two grid
+    _full_step(b)
