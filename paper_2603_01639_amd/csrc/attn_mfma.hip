@@ -1076,14 +1076,14 @@ __global__ void __launch_bounds__(kThreads, 1) attn_stream_kernel(MfmaArgs a) {
 // w_p = 2^(m_p - M) * l_p, M = max_p m_p, over the unit's pieces p in
 // workgroup order, where Ohat_p = O_p / l_p is the piece's normalised output
 // (bf16).  blockIdx.x = the unit (its entry in the merge table says whether it
-// was cut), blockIdx.y picks 16 of its rows: each wave takes 4 rows, 16 lanes
-// per row and 16 bytes (8 dims) per lane.  Lane k of a wave works out the
+// was cut), blockIdx.y picks 64 of its rows: each wave takes 16 rows, 4 lanes
+// per row and 64 bytes (32 dims) per lane.  Lane k of a wave works out the
 // slot of piece k once (64 pieces per round); every lane then walks the
-// pieces in batches of 8 with all their loads in flight, keeping a running
-// max (each batch rescales the sums at most once), so a unit of up to 8
+// pieces in batches of 4 with all their loads in flight, keeping a running
+// max (each batch rescales the sums at most once), so a unit of up to 4
 // pieces takes a single round of loads.
 __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
-  constexpr int kBatch = 8;
+  constexpr int kBatch = 4;
   if (halted(a.status)) return;
   const int units = *reinterpret_cast<const int32_t*>(a.ws_desc);
   const MergeDesc d = a.ws_desc[1 + blockIdx.x];
@@ -1091,10 +1091,10 @@ __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
   const int wv = threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   const int rows = min(a.G * d.n - d.rt * kTileRows, kTileRows);
-  const int r0 = blockIdx.y * 16 + wv * 4;
+  const int r0 = blockIdx.y * 64 + wv * 16;
   if (r0 >= rows) return;
-  const int r = min(r0 + (lane >> 4), rows - 1);  // (rows past the unit's compute its last, unstored)
-  const int col = lane & 15;
+  const int r = min(r0 + (lane >> 2), rows - 1);  // (rows past the unit's compute its last, unstored)
+  const int quarter = lane & 3;                    // dims 32 * quarter .. + 31
   plan::MergeJob job{};
   job.active = true;
   job.sa = d.sa;
@@ -1103,8 +1103,10 @@ __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
   job.u.w = d.w;
   job.q.c.t_pre = d.t_pre;
   const plan::Grid gr = plan::make_grid(d.C, a.W);
-  const int npieces = d.active ? plan::owner(gr, d.U + static_cast<int64_t>(d.w) * d.t_pre) - d.sa + 1 : 0;
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  const int npieces = plan::owner(gr, d.U + static_cast<int64_t>(d.w) * d.t_pre) - d.sa + 1;
+  float acc[32];
+#pragma unroll
+  for (int e = 0; e < 32; ++e) acc[e] = 0.f;
   float wsum = 0.f;
   float M = -INFINITY;  // running max: acc and wsum are relative to 2^M
   for (int c0 = 0; c0 < npieces; c0 += kWave) {
@@ -1112,16 +1114,19 @@ __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
     const int my_slot = lane < cnt ? plan::merge_piece_slot(job, c0 + lane, gr) : -1;
     for (int k0 = 0; k0 < cnt; k0 += kBatch) {
       f32x2 ml[kBatch];
-      u32x4 o[kBatch];
+      u32x4 o[kBatch][4];
 #pragma unroll
       for (int j = 0; j < kBatch; ++j) {
         const int slot = k0 + j < cnt ? __builtin_amdgcn_readlane(my_slot, k0 + j) : -1;
         ml[j] = (f32x2){-INFINITY, 0.f};
-        o[j] = (u32x4){0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) o[j][c] = (u32x4){0u, 0u, 0u, 0u};
         if (slot >= 0) {
           const int64_t row = static_cast<int64_t>(slot) * kTileRows + r;
           ml[j] = *reinterpret_cast<const f32x2*>(a.ws_ml + row * 2);
-          o[j] = *reinterpret_cast<const u32x4*>(a.ws_o + row * kD + col * 8);
+          const u32x4* src = reinterpret_cast<const u32x4*>(a.ws_o + row * kD + quarter * 32);
+#pragma unroll
+          for (int c = 0; c < 4; ++c) o[j][c] = src[c];
         }
       }
       // the batch's pieces join the running sums (one rescale per batch)
@@ -1132,7 +1137,7 @@ __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
         const float alpha = M == -INFINITY ? 0.f : exp2_fast(M - Mb);
         wsum *= alpha;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] *= alpha;
+        for (int e = 0; e < 32; ++e) acc[e] *= alpha;
         M = Mb;
       }
 #pragma unroll
@@ -1140,25 +1145,31 @@ __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
         const float w = ml[j].y > 0.f ? exp2_fast(ml[j].x - M) * ml[j].y : 0.f;
         wsum += w;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc[2 * e] += w * bf16_to_f32(static_cast<uint16_t>(o[j][e] & 0xFFFFu));
-          acc[2 * e + 1] += w * bf16_to_f32(static_cast<uint16_t>(o[j][e] >> 16));
-        }
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc[8 * c + 2 * e] += w * bf16_to_f32(static_cast<uint16_t>(o[j][c][e] & 0xFFFFu));
+            acc[8 * c + 2 * e + 1] += w * bf16_to_f32(static_cast<uint16_t>(o[j][c][e] >> 16));
+          }
       }
     }
   }
-  if (r0 + (lane >> 4) >= rows) return;
+  if (r0 + (lane >> 2) >= rows) return;
   const float inv = 1.f / wsum;
   const int row = d.rt * kTileRows + r;  // stacked row = node * G + head in group
   const int node = row / a.G;
   const int hq = d.g * a.G + row % a.G;
-  uint16_t* orow = a.out + ((static_cast<int64_t>(d.b) * a.Nmax + node) * a.Hq + hq) * kD;
-  u32x4 v;
-  v.x = pack_bf16x2(acc[0] * inv, acc[1] * inv);
-  v.y = pack_bf16x2(acc[2] * inv, acc[3] * inv);
-  v.z = pack_bf16x2(acc[4] * inv, acc[5] * inv);
-  v.w = pack_bf16x2(acc[6] * inv, acc[7] * inv);
-  *reinterpret_cast<u32x4*>(orow + col * 8) = v;
+  u32x4* dst = reinterpret_cast<u32x4*>(
+      a.out + ((static_cast<int64_t>(d.b) * a.Nmax + node) * a.Hq + hq) * kD + quarter * 32);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    u32x4 v;
+    v.x = pack_bf16x2(acc[8 * c + 0] * inv, acc[8 * c + 1] * inv);
+    v.y = pack_bf16x2(acc[8 * c + 2] * inv, acc[8 * c + 3] * inv);
+    v.z = pack_bf16x2(acc[8 * c + 4] * inv, acc[8 * c + 5] * inv);
+    v.w = pack_bf16x2(acc[8 * c + 6] * inv, acc[8 * c + 7] * inv);
+    dst[c] = v;
+  }
 }
 
 }  // namespace
@@ -1390,8 +1401,8 @@ hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q
   hipLaunchKernelGGL(attn_stream_kernel, dim3(p.grid), dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // One merge workgroup column per possible unit, 16 rows per workgroup.
-  hipLaunchKernelGGL(attn_stream_merge_kernel, dim3(a.max_units, kTileRows / 16), dim3(256), 0,
+  // One merge workgroup column per possible unit, 64 rows per workgroup.
+  hipLaunchKernelGGL(attn_stream_merge_kernel, dim3(a.max_units, kTileRows / 64), dim3(256), 0,
                      stream, a);
   return hipGetLastError();
 }
