@@ -96,6 +96,7 @@ struct MfmaArgs {
   uint16_t* out;
   const int32_t* status;
   int B, Nmax, Hq, Hkv, G, kv_rows, max_blocks, max_prefix;
+  int kv_shift;  // log2(kv_rows) when kv_rows is a power of two, else -1
   int W;  // stream plan: workgroups of the grid (a power of two)
   // split plan: prefix keys per split, splits of the longest sequence, whether
   // the tree may take a split of its own, row tiles per (sequence, kv head)
@@ -326,6 +327,10 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   }
   auto row_byte = [&](int row) -> int64_t {  // byte offset of logical cache row `row`
     if (!paged) return ((static_cast<int64_t>(b) * a.Hkv + g) * a.kv_rows + row) * (kD * 2);
+    if (a.kv_shift >= 0) {  // power-of-two blocks: shifts and masks, no division
+      const int64_t blk = sm.blk[(row >> a.kv_shift) - first_blk];
+      return (((blk * a.Hkv + g) << a.kv_shift) + (row & (a.kv_rows - 1))) * (kD * 2);
+    }
     const int64_t blk = sm.blk[row / a.kv_rows - first_blk];
     return ((blk * a.Hkv + g) * a.kv_rows + row % a.kv_rows) * (kD * 2);
   };
@@ -1370,6 +1375,9 @@ hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q
   a.Hkv = s.Hkv;
   a.G = s.Hq / s.Hkv;
   a.kv_rows = s.kv_rows;
+  a.kv_shift = -1;
+  for (int k = 0; k < 31; ++k)
+    if ((1 << k) == s.kv_rows) a.kv_shift = k;
   a.max_blocks = s.max_blocks;
   a.max_prefix = s.max_prefix;
   a.scale_log2 = scale * kLog2e;
