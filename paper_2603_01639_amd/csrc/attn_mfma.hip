@@ -340,11 +340,44 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     k_voff[u] = static_cast<uint32_t>(lp.k_key[u] * (kD * 2) + lp.k_off[u]);
     v_voff[u] = static_cast<uint32_t>(lp.v_key[u] * (kD * 2) + lp.v_off[u]);
   }
+  // Paged caches with power-of-two blocks of at least 4 rows: the 4 keys a
+  // load instruction covers are 4-aligned, so in a full prefix tile (which
+  // starts at a multiple of 64) they lie in one block.  Each instruction then
+  // takes a wave-uniform base, from its block id, in scalar registers, plus a
+  // loop-invariant per-lane offset within the block.
+  const bool paged_uniform = paged && a.kv_shift >= 2;
+  const int in_blk = (a.kv_rows < kKT ? a.kv_rows : kKT) - 1;  // key bits inside a block (of a tile)
+  uint32_t k_poff[kKLoads], v_poff[kKLoads];
+  int k_grp[kKLoads], v_grp[kKLoads];  // first tile key of each instruction (lane 0's)
+#pragma unroll
+  for (int u = 0; u < kKLoads; ++u) {
+    k_poff[u] = static_cast<uint32_t>((lp.k_key[u] & in_blk) * (kD * 2) + lp.k_off[u]);
+    v_poff[u] = static_cast<uint32_t>((lp.v_key[u] & in_blk) * (kD * 2) + lp.v_off[u]);
+    k_grp[u] = __builtin_amdgcn_readfirstlane(lp.k_key[u]);
+    v_grp[u] = __builtin_amdgcn_readfirstlane(lp.v_key[u]);
+  }
   auto issue_tile = [&](int t) {
     const unsigned char* k_s = sm.kv[t % kStages];
     const unsigned char* v_s = k_s + kKBytes;
     const TileRef tr = tile_ref(t);
-    if (!paged && tr.left >= kKT) {
+    if (paged_uniform && !tr.tree && tr.left >= kKT && (tr.row & (kKT - 1)) == 0) {
+      const int64_t in_row = a.kv_rows > kKT ? static_cast<int64_t>(tr.row & (a.kv_rows - 1)) * (kD * 2) : 0;
+      int bk[kKLoads], bv[kKLoads];
+#pragma unroll
+      for (int u = 0; u < kKLoads; ++u) {
+        bk[u] = sm.blk[((tr.row + k_grp[u]) >> a.kv_shift) - first_blk];
+        bv[u] = sm.blk[((tr.row + v_grp[u]) >> a.kv_shift) - first_blk];
+      }
+#pragma unroll
+      for (int u = 0; u < kKLoads; ++u) {
+        const int64_t kb = __builtin_amdgcn_readfirstlane(bk[u]);
+        const int64_t vb = __builtin_amdgcn_readfirstlane(bv[u]);
+        dma16(lds_addr(k_s + lp.lds_pos[u]), kbase + (((kb * a.Hkv + g) << a.kv_shift) * (kD * 2) + in_row),
+              k_poff[u]);
+        dma16(lds_addr(v_s + lp.lds_pos[u]), vbase + (((vb * a.Hkv + g) << a.kv_shift) * (kD * 2) + in_row),
+              v_poff[u]);
+      }
+    } else if (!paged && tr.left >= kKT) {
       // contiguous rows: a uniform tile base plus per-lane 32-bit offsets
       const int64_t base = row_byte(tr.row);
 #pragma unroll
@@ -617,6 +650,10 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
       mask_scores(t, s_acc);
       accumulate(t - 1, pf_prev);  // tile t-1's P.V ...
       exponentials(s_acc, pf);     // ... interleaved with tile t's softmax
+      // (pins P and its row sum ahead of the rescale branch: otherwise the
+      // compiler sinks the exponentials past it, out of reach of the P.V
+      // MFMAs they can overlap)
+      asm volatile("" : "+v"(pf[0][0]), "+v"(pf[0][1]), "+v"(pf[1][0]), "+v"(pf[1][1]), "+v"(psum));
       finish_softmax();            // after P.V(t-1): may rescale O
     }
   };

@@ -237,3 +237,18 @@ def test_batch_of_one_row_blocks_takes_the_split_plan():
     g = ltd.attn_grid(b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix, b.dtype, b.kv_rows, paged=True)
     assert g > 0 and g & (g - 1) != 0  # not the stream plan's power-of-two grid
     _full_step(b)
+
+
+@pytest.mark.parametrize("block_size", [2, 3, 4, 8, 32, 64, 128, 256, 1024])
+@pytest.mark.parametrize("B", [1, 3])
+def test_paged_block_sizes(block_size, B):
+    """Paged caches of many block sizes, one sequence (split plan) and a
+    batch (stream plan): powers of two from 4 rows on take every full prefix
+    tile's loads from one block per load instruction; 2 and 3 rows (and every
+    tree tile or partial tile) address row by row."""
+    rng = np.random.default_rng(100 * block_size + B)
+    nodes = [41, 7, 130][:B]
+    prefix = [1000 + 37 * block_size % 900, 2049, 64][:B]
+    trees = [W.tree_uniform_parent(rng, n) for n in nodes]
+    _full_step(_custom(trees, prefix, Hq=8, Hkv=2, block_size=block_size, seed=block_size + B,
+                       label=f"paged block={block_size} B={B}"))
