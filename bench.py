@@ -410,7 +410,8 @@ def main():
     print(json.dumps(rec), flush=True)
 
 
-EXTRA_WORKLOADS = [("c2", None), ("c3", None)] + [("c4", n) for n in (8, 16, 32, 64, 128, 256)]
+EXTRA_WORKLOADS = ([("c2", None), ("c3", None)] + [("c4", n) for n in (8, 16, 32, 64, 128, 256)]
+                   + [("c2_d64", None)])
 
 
 def workload_key(name, c4_n=None):
@@ -433,6 +434,8 @@ def attention_by_workload(ltd, torch, to_dev, args, graph_of, timed, stream):
             b = W.config2_8b(0, with_logits=False)
         elif name == "c3":
             b = W.config3_long(0, with_logits=False)
+        elif name == "c2_d64":
+            b = W.config2_d64(0, with_logits=False)
         else:
             b = W.config4_sweep(n, min(6, n), with_logits=False)
         attn_bytes, _, flops = algorithmic_bytes(b)
@@ -464,6 +467,9 @@ def attention_by_workload(ltd, torch, to_dev, args, graph_of, timed, stream):
         roof["traffic"] = read_traffic(args.traffic, key, "tree_verify_attn")
         roof["shape"] = (f"B={b.B} Hq={b.Hq} Hkv={b.Hkv} d={b.d} P={int(b.prefix_len[0])} "
                          f"N={int(b.n_nodes[0])}")
+        roof["path"] = ("mfma" if ltd.attn_grid(b.B, b.Nmax, b.Hq, b.Hkv, b.d, b.max_prefix,
+                                                b.dtype, b.kv_rows, paged=b.paged) > 0
+                        else "rowwise")
         out_rows[key] = roof
         del sets, out, ws
         torch.cuda.synchronize()

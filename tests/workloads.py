@@ -366,6 +366,17 @@ def config2_8b(rep: int = 0, with_logits: bool = True) -> VerifyBatch:
                       label="8B bf16 P2048 N60")
 
 
+def config2_d64(rep: int = 0, with_logits: bool = True) -> VerifyBatch:
+    """Config 2's shape with head_dim 64 (32/8 heads, prefix 2048, the same
+    Eagle tree, vocab 128256): the bf16 head size the MFMA kernel does not
+    take, which runs on the row-wise kernel."""
+    rng = rng_for(config_seed(2, rep) + 500)
+    t = tree_eagle(rng, 60, 6, 10, 128256)
+    return make_batch(rng, dtype=DTYPE_BF16, Hq=32, Hkv=8, d=64, prefix=[2048], trees=[t.parents],
+                      tokens=[t.tokens], Voc=128256, p_match=0.7, with_logits=with_logits,
+                      label="8B-shaped bf16 d64 P2048 N60")
+
+
 def config3_long(rep: int = 0, with_logits: bool = True) -> VerifyBatch:
     """As config 2 with prefix 16384 and p=0.8 (long-reasoning context)."""
     rng = rng_for(config_seed(3, rep))
