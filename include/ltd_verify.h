@@ -251,11 +251,13 @@ int ltd_kv_compact(void* k_cache, void* v_cache, const int32_t* block_table,
                    void* stream);
 
 /* Workgroups of the attention launch for a shape and cache layout
- * (kv_rows = capacity or block size, paged != 0 for a block table).  A bf16,
- * head_dim 128 call lays all its (sequence, kv head, row tile) units' key
- * tiles end to end and gives each of that many workgroups an equal share; a
- * unit cut between workgroups is merged by a second kernel.  0 when the call
- * runs on the row-wise kernel instead (fp32 or head_dim 64), -1 on bad args.
+ * (kv_rows = capacity or block size, paged != 0 for a block table).  A bf16
+ * call (head_dim 128 or 64) runs on the matrix-core kernels: a batch lays all
+ * its (sequence, kv head, row tile) units' key tiles end to end and gives each
+ * of that many workgroups (a power of two) an equal share; a single sequence
+ * cuts each unit into KV splits.  Units cut between workgroups are merged by a
+ * second kernel.  0 when the call runs on the row-wise kernel instead (fp32),
+ * -1 on bad args.
  * Introspection for tests and benchmarks. */
 int ltd_tree_verify_attn_grid(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix, int dtype,
                               int kv_rows, int paged);

@@ -1,4 +1,4 @@
-// Split-KV tree attention for bf16 on CDNA4 matrix cores (gfx950), head_dim 128.
+// Split-KV tree attention for bf16 on CDNA4 matrix cores (gfx950), head_dim 128 or 64.
 //
 // What is computed (arXiv 2603.01639, section 3.2): the N draft-tree
 // candidates are verified in one pass, each seeing the KV prefix and its own
@@ -17,7 +17,9 @@
 // workgroup of 8 wavefronts (32 rows each) runs through its share unit by
 // unit.  A unit it covers whole gets its final output written directly; a
 // unit cut between workgroups gets a partial result (max, sum and normalised
-// output) from each of them, which attn_merge_kernel combines.
+// output) from each of them, which attn_stream_merge_kernel combines.  A
+// single sequence instead cuts each unit into KV splits of equal length (the
+// split plan: attn_split_kernel, attn_split_merge_kernel).
 //
 // K/V stream: 64-key tiles move from HBM straight into an LDS ring of
 // kStages slots with global_load_lds_dwordx4 (no register staging); a lane
@@ -38,6 +40,13 @@
 // The ancestor sets of the tree split are built in LDS as N x 256-bit masks by
 // pointer doubling over the parent links: anc(i) = anc(i) | anc(jump(i)),
 // jump(i) = jump(jump(i)), ceil(log2(depth + 1)) <= 8 rounds for N <= 256.
+//
+// Head size: the LDS layouts are those of 128-dim rows (kD) for either size.
+// With 64 dims a row's 8 chunks are fetched into both halves of its LDS row
+// (the lane at chunk c takes global chunk c mod 8 of its swizzled position),
+// and the contractions run over the first 64 dims only: 4 k-steps for S^T and
+// 2 dim blocks for O^T, half the MFMAs of a tile.  Partial results keep the
+// 128-dim row pitch in the workspace.
 #include <algorithm>
 
 #include "ltd_device.hpp"
@@ -58,7 +67,7 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 typedef __attribute__((address_space(3))) void lds_void;
 typedef const __attribute__((address_space(1))) void global_cvoid;
 
-constexpr int kD = 128;                        // head dim
+constexpr int kD = 128;                        // dims of an LDS row (the largest head size)
 constexpr int kKT = 64;                        // keys per tile
 constexpr int kWaves = 8;                      // waves per workgroup
 constexpr int kThreads = kWaves * kWave;
@@ -245,7 +254,7 @@ __device__ __forceinline__ LoadPlan make_load_plan(int wave, int lane) {
 // rest the second; a tile never spans both.  With final_out the share is the
 // whole unit and the normalised output goes to `out`; otherwise the share's
 // partial result goes to workspace slot `slot`.
-template <bool kTree>
+template <bool kTree, int HD>
 __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g, int row0,
                                        int valid_rows, int key_begin, int n_pre, int P, int n,
                                        bool final_out, int slot) {
@@ -294,7 +303,8 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
       const int idx = min(row0 + wave * 32 + R, valid_rows - 1);
       const int lc = (lane & 15) ^ (R & 15);
       const uint16_t* src = a.q +
-          ((static_cast<int64_t>(b) * a.Nmax + idx / a.G) * a.Hq + g * a.G + idx % a.G) * kD + lc * 8;
+          ((static_cast<int64_t>(b) * a.Nmax + idx / a.G) * a.Hq + g * a.G + idx % a.G) * HD +
+          (lc & (HD / 8 - 1)) * 8;
       dma16(lds_addr(q_lds + j * 1024), src);
     }
   }
@@ -326,19 +336,25 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     __syncthreads();
   }
   auto row_byte = [&](int row) -> int64_t {  // byte offset of logical cache row `row`
-    if (!paged) return ((static_cast<int64_t>(b) * a.Hkv + g) * a.kv_rows + row) * (kD * 2);
+    if (!paged) return ((static_cast<int64_t>(b) * a.Hkv + g) * a.kv_rows + row) * (HD * 2);
     if (a.kv_shift >= 0) {  // power-of-two blocks: shifts and masks, no division
       const int64_t blk = sm.blk[(row >> a.kv_shift) - first_blk];
-      return (((blk * a.Hkv + g) << a.kv_shift) + (row & (a.kv_rows - 1))) * (kD * 2);
+      return (((blk * a.Hkv + g) << a.kv_shift) + (row & (a.kv_rows - 1))) * (HD * 2);
     }
     const int64_t blk = sm.blk[row / a.kv_rows - first_blk];
-    return ((blk * a.Hkv + g) * a.kv_rows + row % a.kv_rows) * (kD * 2);
+    return ((blk * a.Hkv + g) * a.kv_rows + row % a.kv_rows) * (HD * 2);
   };
+  // A lane's byte offset of its chunk within a cache row.  The LDS tile keeps
+  // 128-dim rows whatever the head size; with 64 dims each row's 8 chunks
+  // fill both halves of its LDS row (the upper half is never read).
+  int k_off[kKLoads], v_off[kKLoads];
   uint32_t k_voff[kKLoads], v_voff[kKLoads];
 #pragma unroll
   for (int u = 0; u < kKLoads; ++u) {
-    k_voff[u] = static_cast<uint32_t>(lp.k_key[u] * (kD * 2) + lp.k_off[u]);
-    v_voff[u] = static_cast<uint32_t>(lp.v_key[u] * (kD * 2) + lp.v_off[u]);
+    k_off[u] = lp.k_off[u] & (HD * 2 - 1);
+    v_off[u] = lp.v_off[u] & (HD * 2 - 1);
+    k_voff[u] = static_cast<uint32_t>(lp.k_key[u] * (HD * 2) + k_off[u]);
+    v_voff[u] = static_cast<uint32_t>(lp.v_key[u] * (HD * 2) + v_off[u]);
   }
   // Paged caches with power-of-two blocks of at least 4 rows: the 4 keys a
   // load instruction covers are 4-aligned, so in a full prefix tile (which
@@ -351,8 +367,8 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   int k_grp[kKLoads], v_grp[kKLoads];  // first tile key of each instruction (lane 0's)
 #pragma unroll
   for (int u = 0; u < kKLoads; ++u) {
-    k_poff[u] = static_cast<uint32_t>((lp.k_key[u] & in_blk) * (kD * 2) + lp.k_off[u]);
-    v_poff[u] = static_cast<uint32_t>((lp.v_key[u] & in_blk) * (kD * 2) + lp.v_off[u]);
+    k_poff[u] = static_cast<uint32_t>((lp.k_key[u] & in_blk) * (HD * 2) + k_off[u]);
+    v_poff[u] = static_cast<uint32_t>((lp.v_key[u] & in_blk) * (HD * 2) + v_off[u]);
     k_grp[u] = __builtin_amdgcn_readfirstlane(lp.k_key[u]);
     v_grp[u] = __builtin_amdgcn_readfirstlane(lp.v_key[u]);
   }
@@ -361,7 +377,7 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     const unsigned char* v_s = k_s + kKBytes;
     const TileRef tr = tile_ref(t);
     if (paged_uniform && !tr.tree && tr.left >= kKT && (tr.row & (kKT - 1)) == 0) {
-      const int64_t in_row = a.kv_rows > kKT ? static_cast<int64_t>(tr.row & (a.kv_rows - 1)) * (kD * 2) : 0;
+      const int64_t in_row = a.kv_rows > kKT ? static_cast<int64_t>(tr.row & (a.kv_rows - 1)) * (HD * 2) : 0;
       int bk[kKLoads], bv[kKLoads];
 #pragma unroll
       for (int u = 0; u < kKLoads; ++u) {
@@ -372,9 +388,9 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
       for (int u = 0; u < kKLoads; ++u) {
         const int64_t kb = __builtin_amdgcn_readfirstlane(bk[u]);
         const int64_t vb = __builtin_amdgcn_readfirstlane(bv[u]);
-        dma16(lds_addr(k_s + lp.lds_pos[u]), kbase + (((kb * a.Hkv + g) << a.kv_shift) * (kD * 2) + in_row),
+        dma16(lds_addr(k_s + lp.lds_pos[u]), kbase + (((kb * a.Hkv + g) << a.kv_shift) * (HD * 2) + in_row),
               k_poff[u]);
-        dma16(lds_addr(v_s + lp.lds_pos[u]), vbase + (((vb * a.Hkv + g) << a.kv_shift) * (kD * 2) + in_row),
+        dma16(lds_addr(v_s + lp.lds_pos[u]), vbase + (((vb * a.Hkv + g) << a.kv_shift) * (HD * 2) + in_row),
               v_poff[u]);
       }
     } else if (!paged && tr.left >= kKT) {
@@ -392,8 +408,8 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
       for (int u = 0; u < kKLoads; ++u) {
         const int kk = tr.row + min(lp.k_key[u], tr.left - 1);
         const int vk = tr.row + min(lp.v_key[u], tr.left - 1);
-        dma16(lds_addr(k_s + lp.lds_pos[u]), kbase + row_byte(kk) + lp.k_off[u]);
-        dma16(lds_addr(v_s + lp.lds_pos[u]), vbase + row_byte(vk) + lp.v_off[u]);
+        dma16(lds_addr(k_s + lp.lds_pos[u]), kbase + row_byte(kk) + k_off[u]);
+        dma16(lds_addr(v_s + lp.lds_pos[u]), vbase + row_byte(vk) + v_off[u]);
       }
     }
   };
@@ -414,10 +430,10 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   // ---- Q fragment (B operand of S^T): lane holds row l32 of the wave's
   // 32-row block, dims 16*kk + 8*h .. +7.  All waves have read theirs before
   // the loop's first barrier, after which tile 2 overwrites the slot.
-  bf16x8 qf[kD / 16];
+  bf16x8 qf[HD / 16];
   if (active) {
 #pragma unroll
-    for (int kk = 0; kk < kD / 16; ++kk)
+    for (int kk = 0; kk < HD / 16; ++kk)
       qf[kk] = *reinterpret_cast<const bf16x8*>(q_lds + l32 * (kD * 2) +
                                                 (((2 * kk + h) ^ (l32 & 15)) << 4));
   }
@@ -490,36 +506,36 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
 
   // ---- online softmax state (raw score units) and O^T accumulators
   float m_run = -INFINITY, l_run = 0.f;
-  f32x16 o_acc[kD / 32];
+  f32x16 o_acc[HD / 32];
 #pragma unroll
-  for (int db = 0; db < kD / 32; ++db) o_acc[db] = f32x16{};
+  for (int db = 0; db < HD / 32; ++db) o_acc[db] = f32x16{};
   const float c = a.scale_log2;
 
   // LDS read offsets (bytes within a tile), all loop-invariant:
   //  K operand, 16-dim step kk: row l32 of the 32-row block, chunk
   //  (2*kk + h) ^ (l32 & 15).
-  int k_rd[kD / 16];
+  int k_rd[HD / 16];
 #pragma unroll
-  for (int kk = 0; kk < kD / 16; ++kk)
+  for (int kk = 0; kk < HD / 16; ++kk)
     k_rd[kk] = l32 * (kD * 2) + (((2 * kk + h) ^ (l32 & 15)) << 4);
   //  V^T operand: 16-lane group q reads key 16*(q/2) + s/4 (+ the k-step's
   //  base, a multiple of 4), dims 32*db + 16*(q%2) + 4*(s%4).
   const int tr_q = lane >> 4, tr_s = lane & 15;
   const int tr_key = 16 * (tr_q >> 1) + (tr_s >> 2);
-  int v_rd[kD / 32];
+  int v_rd[HD / 32];
 #pragma unroll
-  for (int db = 0; db < kD / 32; ++db) {
+  for (int db = 0; db < HD / 32; ++db) {
     const int dim = 32 * db + 16 * (tr_q & 1) + 4 * (tr_s & 3);
     v_rd[db] = tr_key * (kD * 2) + (((dim >> 3) ^ swz_v(tr_key)) << 4) + (dim & 7) * 2;
   }
 
   // K fragments of a tile (A operand of S^T), read into registers one phase
   // ahead of their MFMAs.
-  bf16x8 af[2][kD / 16];
+  bf16x8 af[2][HD / 16];
   auto load_k = [&](int t) {
     const unsigned char* k_s = sm.kv[t % kStages];
 #pragma unroll
-    for (int kk = 0; kk < kD / 16; ++kk)
+    for (int kk = 0; kk < HD / 16; ++kk)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
         af[kb][kk] = *reinterpret_cast<const bf16x8*>(k_s + kb * 32 * (kD * 2) + k_rd[kk]);
@@ -528,7 +544,7 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   auto scores = [&](f32x16(&s)[2]) {
     s[0] = s[1] = f32x16{};
 #pragma unroll
-    for (int kk = 0; kk < kD / 16; ++kk)
+    for (int kk = 0; kk < HD / 16; ++kk)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kb][kk], qf[kk], s[kb], 0, 0, 0);
@@ -597,7 +613,7 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
       const float alpha = (m_new == -INFINITY) ? 1.f : exp2_fast((m_run - m_new) * c);
       l_run *= alpha;
 #pragma unroll
-      for (int db = 0; db < kD / 32; ++db) o_acc[db] *= alpha;
+      for (int db = 0; db < HD / 32; ++db) o_acc[db] *= alpha;
     }
     l_run += psum;
     m_run = m_new;
@@ -610,15 +626,15 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
 #pragma unroll
     for (int kc = 0; kc < 4; ++kc) {
       const int koff = (32 * (kc >> 1) + 8 * (kc & 1)) * (kD * 2);
-      bf16x8 vf[kD / 32];
+      bf16x8 vf[HD / 32];
 #pragma unroll
-      for (int db = 0; db < kD / 32; ++db) {
+      for (int db = 0; db < HD / 32; ++db) {
         const s16x4 lo = lds_read_tr(v_s + v_rd[db] + koff);
         const s16x4 hi = lds_read_tr(v_s + v_rd[db] + koff + 4 * (kD * 2));
         vf[db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       }
 #pragma unroll
-      for (int db = 0; db < kD / 32; ++db)
+      for (int db = 0; db < HD / 32; ++db)
         o_acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db], pf[kc >> 1][kc & 1], o_acc[db], 0, 0, 0);
     }
   };
@@ -702,7 +718,7 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
     unsigned char* srow = stage + l32 * kRowPitch;
 #pragma unroll
-    for (int db = 0; db < kD / 32; ++db) {
+    for (int db = 0; db < HD / 32; ++db) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         uint2 v;
@@ -715,7 +731,9 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  constexpr int kChunks = 32 * (kD * 2 / 16);  // 16-byte chunks of this wave's rows
+  constexpr int kRowChunks = HD * 2 / 16;       // 16-byte chunks of an output row
+  constexpr int kChunks = 32 * kRowChunks;       // ... of this wave's rows
+  static_assert(kChunks % kWave == 0, "whole store rounds");
   const int wrow0 = row0 + wave * 32;
   // (an opaque copy of the lane index: otherwise the compiler shares the
   // chunk indices below with the parent-link loads before the tile loop and
@@ -727,11 +745,11 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
 #pragma unroll
     for (int i = 0; i < kChunks / kWave; ++i) {
       const int cidx = i * kWave + lane_e;
-      const int r = cidx >> 4, col = cidx & 15;
+      const int r = cidx / kRowChunks, col = cidx % kRowChunks;
       const int row = wrow0 + r;
       if (row < valid_rows) {
         uint16_t* orow =
-            a.out + ((static_cast<int64_t>(b) * a.Nmax + row / a.G) * a.Hq + g * a.G + row % a.G) * kD;
+            a.out + ((static_cast<int64_t>(b) * a.Nmax + row / a.G) * a.Hq + g * a.G + row % a.G) * HD;
         *reinterpret_cast<u32x4*>(orow + col * 8) =
             *reinterpret_cast<const u32x4*>(stage + r * kRowPitch + col * 16);
       }
@@ -742,7 +760,7 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
 #pragma unroll
   for (int i = 0; i < kChunks / kWave; ++i) {
     const int cidx = i * kWave + lane_e;
-    const int r = cidx >> 4, col = cidx & 15;
+    const int r = cidx / kRowChunks, col = cidx % kRowChunks;
     if (wrow0 + r < valid_rows)
       __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(stage + r * kRowPitch + col * 16),
                                   reinterpret_cast<u32x4*>(gbase + r * (kD * 2) + col * 16));
@@ -910,6 +928,7 @@ __device__ __forceinline__ int stream_index(int w, int W) { return (w % 8) * (W 
 // share one XCD (its L2 holds their common Q rows and K/V).  A unit with one
 // split writes its output directly; otherwise split sp leaves its partial in
 // slot (bg * max_splits + sp) * row_tiles + row tile.
+template <int HD>
 __global__ void __launch_bounds__(kThreads, 1) attn_split_kernel(MfmaArgs a) {
   __shared__ __attribute__((aligned(16))) Smem sm;
   const int bg = blockIdx.x;
@@ -931,9 +950,9 @@ __global__ void __launch_bounds__(kThreads, 1) attn_split_kernel(MfmaArgs a) {
   const int n_pre = min(a.split_keys, P - key_begin);
   const int slot = (bg * a.max_splits + split) * a.row_tiles + rtile;
   if (split == nsp - 1)
-    attend<true>(a, sm, b, g, row0, valid_rows, key_begin, n_pre, P, n, nsp == 1, slot);
+    attend<true, HD>(a, sm, b, g, row0, valid_rows, key_begin, n_pre, P, n, nsp == 1, slot);
   else
-    attend<false>(a, sm, b, g, row0, valid_rows, key_begin, n_pre, P, n, nsp == 1, slot);
+    attend<false, HD>(a, sm, b, g, row0, valid_rows, key_begin, n_pre, P, n, nsp == 1, slot);
 }
 
 // Split plan merge, one wave per stacked row: combine the splits' partials
@@ -946,6 +965,7 @@ __global__ void __launch_bounds__(kThreads, 1) attn_split_kernel(MfmaArgs a) {
 // requested before the sequence's prefix length and node count arrive: every
 // row of the grid is inside the workspace's Mpad rows, and every split index
 // below max_splits inside its splits.
+template <int HD>
 __global__ void __launch_bounds__(256) attn_split_merge_kernel(MfmaArgs a) {
   __shared__ float w_s[4][kMaxMergeSplits];
   constexpr int kFirst = 16;  // splits whose rows are requested up front
@@ -1025,11 +1045,11 @@ __global__ void __launch_bounds__(256) attn_split_merge_kernel(MfmaArgs a) {
     acc[e] += __shfl_xor(acc[e], 16, kWave);
     acc[e] += __shfl_xor(acc[e], 32, kWave);
   }
-  if (grp == 0) {
+  if (grp == 0 && col < HD / 8) {  // (lanes past the head's dims summed unused workspace)
     const float inv = 1.f / wsum;
     const int node = row / a.G;
     const int hq = g * a.G + row % a.G;
-    uint16_t* orow = a.out + ((static_cast<int64_t>(b) * a.Nmax + node) * a.Hq + hq) * kD;
+    uint16_t* orow = a.out + ((static_cast<int64_t>(b) * a.Nmax + node) * a.Hq + hq) * HD;
     u32x4 v;
     v.x = pack_bf16x2(acc[0] * inv, acc[1] * inv);
     v.y = pack_bf16x2(acc[2] * inv, acc[3] * inv);
@@ -1044,6 +1064,7 @@ __global__ void __launch_bounds__(256) attn_split_merge_kernel(MfmaArgs a) {
 // into LDS, then run one by one by the whole workgroup: the partition's state
 // (the sequence table, positions) is dead while the tile loop runs, which
 // keeps it out of the loop's registers.
+template <int HD>
 __global__ void __launch_bounds__(kThreads, 1) attn_stream_kernel(MfmaArgs a) {
   __shared__ __attribute__((aligned(16))) Smem sm;
   if (halted(a.status)) return;
@@ -1103,10 +1124,10 @@ __global__ void __launch_bounds__(kThreads, 1) attn_stream_kernel(MfmaArgs a) {
       const ShareDesc d = sm.share[i];
       const int row0 = d.rt * kTileRows;
       if (d.tree)
-        attend<true>(a, sm, d.b, d.g, row0, a.G * d.n, d.key_begin, d.n_pre, d.P, d.n,
+        attend<true, HD>(a, sm, d.b, d.g, row0, a.G * d.n, d.key_begin, d.n_pre, d.P, d.n,
                      d.whole != 0, d.slot);
       else
-        attend<false>(a, sm, d.b, d.g, row0, a.G * d.n, d.key_begin, d.n_pre, d.P, d.n,
+        attend<false, HD>(a, sm, d.b, d.g, row0, a.G * d.n, d.key_begin, d.n_pre, d.P, d.n,
                       d.whole != 0, d.slot);
     }
     if (next_pos < 0) break;
@@ -1119,13 +1140,16 @@ __global__ void __launch_bounds__(kThreads, 1) attn_stream_kernel(MfmaArgs a) {
 // workgroup order, where Ohat_p = O_p / l_p is the piece's normalised output
 // (bf16).  blockIdx.x = the unit (its entry in the merge table says whether it
 // was cut), blockIdx.y picks 64 of its rows: each wave takes 16 rows, 4 lanes
-// per row and 64 bytes (32 dims) per lane.  Lane k of a wave works out the
+// per row and a quarter of the head's dims per lane.  Lane k of a wave works out the
 // slot of piece k once (64 pieces per round); every lane then walks the
 // pieces in batches of 4 with all their loads in flight, keeping a running
 // max (each batch rescales the sums at most once), so a unit of up to 4
 // pieces takes a single round of loads.
+template <int HD>
 __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
   constexpr int kBatch = 4;
+  constexpr int kQD = HD / 4;       // dims per lane (4 lanes per row)
+  constexpr int kQC = kQD / 8;      // 16-byte chunks per lane
   if (halted(a.status)) return;
   const int units = *reinterpret_cast<const int32_t*>(a.ws_desc);
   const MergeDesc d = a.ws_desc[1 + blockIdx.x];
@@ -1136,7 +1160,7 @@ __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
   const int r0 = blockIdx.y * 64 + wv * 16;
   if (r0 >= rows) return;
   const int r = min(r0 + (lane >> 2), rows - 1);  // (rows past the unit's compute its last, unstored)
-  const int quarter = lane & 3;                    // dims 32 * quarter .. + 31
+  const int quarter = lane & 3;                    // dims kQD * quarter .. + kQD - 1
   plan::MergeJob job{};
   job.active = true;
   job.sa = d.sa;
@@ -1146,9 +1170,9 @@ __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
   job.q.c.t_pre = d.t_pre;
   const plan::Grid gr = plan::make_grid(d.C, a.W);
   const int npieces = plan::owner(gr, d.U + static_cast<int64_t>(d.w) * d.t_pre) - d.sa + 1;
-  float acc[32];
+  float acc[kQD];
 #pragma unroll
-  for (int e = 0; e < 32; ++e) acc[e] = 0.f;
+  for (int e = 0; e < kQD; ++e) acc[e] = 0.f;
   float wsum = 0.f;
   float M = -INFINITY;  // running max: acc and wsum are relative to 2^M
   for (int c0 = 0; c0 < npieces; c0 += kWave) {
@@ -1156,19 +1180,19 @@ __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
     const int my_slot = lane < cnt ? plan::merge_piece_slot(job, c0 + lane, gr) : -1;
     for (int k0 = 0; k0 < cnt; k0 += kBatch) {
       f32x2 ml[kBatch];
-      u32x4 o[kBatch][4];
+      u32x4 o[kBatch][kQC];
 #pragma unroll
       for (int j = 0; j < kBatch; ++j) {
         const int slot = k0 + j < cnt ? __builtin_amdgcn_readlane(my_slot, k0 + j) : -1;
         ml[j] = (f32x2){-INFINITY, 0.f};
 #pragma unroll
-        for (int c = 0; c < 4; ++c) o[j][c] = (u32x4){0u, 0u, 0u, 0u};
+        for (int c = 0; c < kQC; ++c) o[j][c] = (u32x4){0u, 0u, 0u, 0u};
         if (slot >= 0) {
           const int64_t row = static_cast<int64_t>(slot) * kTileRows + r;
           ml[j] = *reinterpret_cast<const f32x2*>(a.ws_ml + row * 2);
-          const u32x4* src = reinterpret_cast<const u32x4*>(a.ws_o + row * kD + quarter * 32);
+          const u32x4* src = reinterpret_cast<const u32x4*>(a.ws_o + row * kD + quarter * kQD);
 #pragma unroll
-          for (int c = 0; c < 4; ++c) o[j][c] = src[c];
+          for (int c = 0; c < kQC; ++c) o[j][c] = src[c];
         }
       }
       // the batch's pieces join the running sums (one rescale per batch)
@@ -1179,7 +1203,7 @@ __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
         const float alpha = M == -INFINITY ? 0.f : exp2_fast(M - Mb);
         wsum *= alpha;
 #pragma unroll
-        for (int e = 0; e < 32; ++e) acc[e] *= alpha;
+        for (int e = 0; e < kQD; ++e) acc[e] *= alpha;
         M = Mb;
       }
 #pragma unroll
@@ -1187,7 +1211,7 @@ __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
         const float w = ml[j].y > 0.f ? exp2_fast(ml[j].x - M) * ml[j].y : 0.f;
         wsum += w;
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
+        for (int c = 0; c < kQC; ++c)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             acc[8 * c + 2 * e] += w * bf16_to_f32(static_cast<uint16_t>(o[j][c][e] & 0xFFFFu));
@@ -1202,9 +1226,9 @@ __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
   const int node = row / a.G;
   const int hq = d.g * a.G + row % a.G;
   u32x4* dst = reinterpret_cast<u32x4*>(
-      a.out + ((static_cast<int64_t>(d.b) * a.Nmax + node) * a.Hq + hq) * kD + quarter * 32);
+      a.out + ((static_cast<int64_t>(d.b) * a.Nmax + node) * a.Hq + hq) * HD + quarter * kQD);
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
+  for (int c = 0; c < kQC; ++c) {
     u32x4 v;
     v.x = pack_bf16x2(acc[8 * c + 0] * inv, acc[8 * c + 1] * inv);
     v.y = pack_bf16x2(acc[8 * c + 2] * inv, acc[8 * c + 3] * inv);
@@ -1367,7 +1391,7 @@ void plan_split(const AttnShape& s, int num_cus, AttnPlan* p) {
 // The split plan needs splits of at least two key tiles whose block ids fit
 // the LDS table even with one-row blocks, and at most kMaxMergeSplits of them.
 bool mfma_supported(const AttnShape& s) {
-  if (s.dtype != LTD_DTYPE_BF16 || s.d != kD) return false;
+  if (s.dtype != LTD_DTYPE_BF16 || (s.d != 128 && s.d != 64)) return false;
   if (use_stream(s)) return true;
   const int64_t cap = worst_split_key_cap(s);
   return cap >= 2 * kKT && s.max_prefix <= cap * kMaxMergeSplits;
@@ -1429,13 +1453,19 @@ hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q
     const size_t slots = static_cast<size_t>(s.B) * s.Hkv * p.max_splits * p.row_tiles * kTileRows;
     a.ws_ml = reinterpret_cast<float*>(ws + slots * kD * 2);
     const dim3 grid(s.B * s.Hkv, p.row_tiles, p.max_splits);
-    hipLaunchKernelGGL(attn_split_kernel, grid, dim3(kThreads), 0, stream, a);
+    if (s.d == 64)
+      hipLaunchKernelGGL(attn_split_kernel<64>, grid, dim3(kThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL(attn_split_kernel<128>, grid, dim3(kThreads), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.max_splits == 1) return e;  // one split: the output is final
     // (sequence, kv head) fastest, as for the attention grid: a head's merge
     // runs on the XCD whose workgroups wrote its partials.
     const dim3 mgrid(s.B * s.Hkv, static_cast<unsigned>((p.row_tiles * kTileRows + 3) / 4));
-    hipLaunchKernelGGL(attn_split_merge_kernel, mgrid, dim3(256), 0, stream, a);
+    if (s.d == 64)
+      hipLaunchKernelGGL(attn_split_merge_kernel<64>, mgrid, dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL(attn_split_merge_kernel<128>, mgrid, dim3(256), 0, stream, a);
     return hipGetLastError();
   }
   const size_t slots = static_cast<size_t>(2) * p.grid * kTileRows;
@@ -1443,12 +1473,19 @@ hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q
   a.ws_desc = reinterpret_cast<MergeDesc*>(ws + slots * (kD * 2 + 2 * sizeof(float)));
   a.W = p.grid;
   a.max_units = static_cast<int>(max_units(s));
-  hipLaunchKernelGGL(attn_stream_kernel, dim3(p.grid), dim3(kThreads), 0, stream, a);
+  if (s.d == 64)
+    hipLaunchKernelGGL(attn_stream_kernel<64>, dim3(p.grid), dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(attn_stream_kernel<128>, dim3(p.grid), dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // One merge workgroup column per possible unit, 64 rows per workgroup.
-  hipLaunchKernelGGL(attn_stream_merge_kernel, dim3(a.max_units, kTileRows / 64), dim3(256), 0,
-                     stream, a);
+  if (s.d == 64)
+    hipLaunchKernelGGL(attn_stream_merge_kernel<64>, dim3(a.max_units, kTileRows / 64), dim3(256),
+                       0, stream, a);
+  else
+    hipLaunchKernelGGL(attn_stream_merge_kernel<128>, dim3(a.max_units, kTileRows / 64), dim3(256),
+                       0, stream, a);
   return hipGetLastError();
 }
 

@@ -71,8 +71,8 @@ def test_bf16_head128_workloads_plan_the_mfma_grid():
     two key tiles and gives the 60-node tree a split of its own (8 x 17
     workgroups).  A batch takes the stream plan: a power of two of at least 8
     workgroups (one eighth of the work per XCD), at most one per compute unit,
-    two partial slots each.  fp32 and head_dim 64 run on the row-wise kernel
-    (grid 0, no workspace)."""
+    two partial slots each.  bf16 head_dim 64 takes the same plans as 128;
+    fp32 runs on the row-wise kernel (grid 0, no workspace)."""
     assert ltd.attn_grid(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 2108) == 8 * 17
     for P, N, Hq in ((16384, 60, 32), (4096, 256, 64), (4096, 8, 64)):
         g = ltd.attn_grid(1, N, Hq, 8, 128, P, ltd.DTYPE_BF16, P + N)
@@ -92,7 +92,9 @@ def test_bf16_head128_workloads_plan_the_mfma_grid():
     assert g > 0 and g % 16 == 0 and g & (g - 1) != 0
     assert ltd.attn_grid(2, 64, 8, 8, 128, 200000, ltd.DTYPE_BF16, 16, paged=True) == 256
     assert ltd.attn_grid(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32, 144) == 0
-    assert ltd.attn_grid(1, 16, 8, 8, 64, 128, ltd.DTYPE_BF16, 144) == 0
+    for B, P in ((1, 128), (1, 2048), (3, 2048)):
+        g64 = ltd.attn_grid(B, 16, 8, 8, 64, P, ltd.DTYPE_BF16, P + 16)
+        assert g64 > 0 and g64 == ltd.attn_grid(B, 16, 8, 8, 128, P, ltd.DTYPE_BF16, P + 16)
     assert ltd.attn_workspace_size(1, 16, 8, 8, 64, 128, ltd.DTYPE_F32) == 0
 
 

@@ -252,3 +252,24 @@ def test_paged_block_sizes(block_size, B):
     trees = [W.tree_uniform_parent(rng, n) for n in nodes]
     _full_step(_custom(trees, prefix, Hq=8, Hkv=2, block_size=block_size, seed=block_size + B,
                        label=f"paged block={block_size} B={B}"))
+
+
+@pytest.mark.parametrize("rep", range(3))
+def test_config2_head_dim_64(rep):
+    """Config 2's shape with head_dim 64: the matrix-core kernels over the
+    first 64 dims of their 128-dim LDS rows (split plan)."""
+    _full_step(W.config2_d64(rep))
+
+
+@pytest.mark.parametrize("block_size", [0, 3, 4, 16, 256])
+def test_head_dim_64_batches(block_size):
+    """bf16 head_dim 64 batches on the stream plan, contiguous and paged (row
+    by row for 3-row blocks, one block per load instruction from 4 rows on),
+    with ragged prefixes and trees, a grouped and an ungrouped head layout."""
+    rng = np.random.default_rng(640 + block_size)
+    trees = [W.tree_uniform_parent(rng, n) for n in (60, 1, 200, 33)]
+    _full_step(_custom(trees, [2049, 5, 700, 64], Hq=16, Hkv=4, d=64, block_size=block_size,
+                       seed=640 + block_size, label=f"d64 batch block={block_size}"))
+    trees = [W.tree_uniform_parent(rng, n) for n in (17, 90)]
+    _full_step(_custom(trees, [1000, 3000], Hq=4, Hkv=4, d=64, block_size=block_size,
+                       seed=641 + block_size, label=f"d64 G=1 block={block_size}"))
