@@ -1169,7 +1169,7 @@ __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
   job.u.w = d.w;
   job.q.c.t_pre = d.t_pre;
   const plan::Grid gr = plan::make_grid(d.C, a.W);
-  const int npieces = plan::owner(gr, d.U + static_cast<int64_t>(d.w) * d.t_pre) - d.sa + 1;
+  const int npieces = plan::owner(gr, plan::tree_item(d.U, d.w, d.t_pre)) - d.sa + 1;
   float acc[kQD];
 #pragma unroll
   for (int e = 0; e < kQD; ++e) acc[e] = 0.f;
@@ -1260,7 +1260,10 @@ int64_t max_units(const AttnShape& s) {
 bool share_fits(const AttnShape& s, int W) {
   if (s.max_blocks <= 0) return true;  // contiguous cache: no table
   const int64_t unit_rows = static_cast<int64_t>(s.max_prefix) + s.Nmax;
-  const int64_t axis_tiles = max_units(s) * max_unit_tiles(s) * plan::tile_weight(8);
+  const int64_t axis_tiles =
+      max_units(s) *
+      plan::unit_extent(static_cast<int>((s.max_prefix + kKT - 1) / kKT), (s.Nmax + kKT - 1) / kKT) *
+      plan::tile_weight(8);
   const int64_t share_rows =
       std::min(unit_rows, (axis_tiles / W / 2 + 2) * kKT + static_cast<int64_t>(s.Nmax));
   return share_rows / s.kv_rows + 2 <= kMaxSplitBlocks;

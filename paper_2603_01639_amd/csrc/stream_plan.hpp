@@ -6,11 +6,14 @@
 // prefix key tiles j = 0 .. T_pre - 1 (64 keys each) and then one tree block
 // (the tree's ceil(n / 64) key tiles under the ancestor mask, never cut).
 // Units are listed sequence by sequence, kv head by kv head, row tile by row
-// tile, and laid end to end on one axis where an item of a unit that starts
-// at U with per-tile weight wu sits at U + wu * j (the tree block at
-// U + wu * T_pre) and the unit ends at U + wu * (T_pre + T_tree).  The weight
-// prices a tile by the waves that compute on it: a row tile with few valid
-// rows streams the same keys with fewer waves busy and costs less per tile.
+// tile, and laid end to end on one axis.  A unit that starts at U with
+// per-tile weight wu first takes wu * kUnitOverhead for the fixed cost of a
+// piece (its Q rows and first tiles in flight, the output written at the
+// end); its items start at I = U + wu * kUnitOverhead, item j at I + wu * j,
+// the tree block at I + wu * T_pre, and the unit ends at
+// I + wu * (T_pre + kTreeCost * T_tree).  The weight prices a tile by the
+// waves that compute on it: a row tile with few valid rows streams the same
+// keys with fewer waves busy and costs less per tile.
 //
 // With C the axis length and W workgroups, workgroup s owns the items whose
 // position p has floor(p * W / C) == s: a contiguous run of the unit list.
@@ -33,9 +36,20 @@ constexpr int kKeyTile = 64;    // keys per tile
 constexpr int kUnitRows = 256;  // stacked query rows per unit (8 waves x 32)
 constexpr int kWaveRows = 32;
 
-// Relative cost of one key tile for a row tile with v busy waves (measured:
-// about 2.3 us per tile with 5-8 waves, 1.7 us with 2-4, 1.0 us with one).
-constexpr int tile_weight(int waves) { return waves >= 5 ? 4 : (waves >= 2 ? 3 : 2); }
+// Relative cost of one key tile for a row tile with v busy waves (measured
+// with per-workgroup timestamps on a batch of 16 sequences: about 2.3 us per
+// tile with 5-8 waves, 1.6 us with 1-4).
+constexpr int tile_weight(int waves) { return waves >= 5 ? 3 : 2; }
+// Axis extent of a tree key tile in prefix tiles (the ancestor masks are built
+// and applied on them: about 6.5 us per tree tile with 5-8 waves), and of a
+// piece's fixed cost (about 4.5 us before the first tile and 2 us after the
+// last one).
+constexpr int kTreeCost = 3;
+constexpr int kUnitOverhead = 2;
+// A unit's axis extent in units of its tile weight.
+constexpr int64_t unit_extent(int t_pre, int t_tree) {
+  return kUnitOverhead + static_cast<int64_t>(t_pre) + static_cast<int64_t>(kTreeCost) * t_tree;
+}
 
 struct SeqCost {
   int rt;      // row tiles (units per kv head)
@@ -57,7 +71,7 @@ constexpr SeqCost seq_cost(int P, int n, int G) {
   c.w_last = c.rt > 0 ? tile_weight((last_rows + kWaveRows - 1) / kWaveRows) : 0;
   c.t_pre = (P + kKeyTile - 1) / kKeyTile;
   c.t_tree = (n + kKeyTile - 1) / kKeyTile;
-  const int64_t tiles = c.t_pre + c.t_tree;
+  const int64_t tiles = unit_extent(c.t_pre, c.t_tree);
   c.per_head = c.rt > 0 ? (static_cast<int64_t>(c.rt - 1) * c.w_full + c.w_last) * tiles : 0;
   return c;
 }
@@ -75,7 +89,7 @@ struct Unit {
 // steps, and most calls take one or two.)
 constexpr Unit locate(int64_t off, const SeqCost& c) {
   Unit u{};
-  const int64_t tiles = c.t_pre + c.t_tree;
+  const int64_t tiles = unit_extent(c.t_pre, c.t_tree);
   const int64_t full = c.w_full * tiles;  // axis length of a full row tile
   int64_t in_head = off;
   u.g = 0;
@@ -128,6 +142,7 @@ struct Share {
 };
 // ceil(max(x, 0) / w) for an item offset x and a tile weight w in {2, 3, 4},
 // clamped to `cap` items (shifts, and a multiply by ceil(2^33 / 3) for w = 3).
+// x counts from the unit's first item I.
 constexpr int item_index(int64_t x, int w, int cap) {
   if (x <= 0) return 0;
   const int64_t lim = static_cast<int64_t>(cap) * w;
@@ -136,13 +151,16 @@ constexpr int item_index(int64_t x, int w, int cap) {
   if (w == 2) return static_cast<int>(xi >> 1);
   return static_cast<int>((static_cast<uint64_t>(xi) * 0xAAAAAAABull) >> 33);
 }
+// Axis position of the first item of a unit that starts at U.
+constexpr int64_t first_item(int64_t U, int w) { return U + static_cast<int64_t>(w) * kUnitOverhead; }
 constexpr Share share_of(int64_t U, int w, int t_pre, int64_t lo, int64_t hi) {
   Share s{};
-  const int a = item_index(lo - U, w, t_pre + 1);  // first item index at or after lo
-  const int b = item_index(hi - U, w, t_pre + 1);  // first item index at or after hi
+  const int64_t I = first_item(U, w);
+  const int a = item_index(lo - I, w, t_pre + 1);  // first item index at or after lo
+  const int b = item_index(hi - I, w, t_pre + 1);  // first item index at or after hi
   s.j0 = a < t_pre ? a : t_pre;
   s.j1 = b < t_pre ? b : t_pre;
-  const int64_t tree_pos = U + static_cast<int64_t>(w) * t_pre;
+  const int64_t tree_pos = I + static_cast<int64_t>(w) * t_pre;
   s.tree = lo <= tree_pos && tree_pos < hi;
   return s;
 }
@@ -177,7 +195,11 @@ struct SeqAt {
 constexpr int unit_index(const SeqAt& q, const Unit& u) { return q.ubase + u.g * q.c.rt + u.rt; }
 
 constexpr int64_t unit_end(const SeqAt& q, const Unit& u) {
-  return q.pre + u.start + static_cast<int64_t>(u.w) * (q.c.t_pre + q.c.t_tree);
+  return q.pre + u.start + static_cast<int64_t>(u.w) * unit_extent(q.c.t_pre, q.c.t_tree);
+}
+// Axis position of a unit's tree block (its last item).
+constexpr int64_t tree_item(int64_t U, int w, int t_pre) {
+  return first_item(U, w) + static_cast<int64_t>(w) * t_pre;
 }
 
 // Workgroup s's shares, in order, from axis position `pos` (its range start,
@@ -199,7 +221,7 @@ constexpr int64_t walk_shares(int s, const Grid& gr, int64_t pos, bool& first, i
     const int64_t U = q.pre + u.start;
     const Share sh = share_of(U, u.w, q.c.t_pre, lo, hi);
     if (!sh.empty()) {
-      visit(q, u, U, sh, U >= lo && sh.j0 == 0 && sh.tree, piece_slot(s, first));
+      visit(q, u, U, sh, first_item(U, u.w) >= lo && sh.j0 == 0 && sh.tree, piece_slot(s, first));
       first = false;
       ++visited;
     }
@@ -219,7 +241,8 @@ constexpr void for_each_share(int s, const Grid& gr, Find find, Visit visit) {
 // The merge of a unit, worked out by the workgroup s that owns the unit's tree
 // block (its last item, so every unit has exactly one such workgroup).  The
 // unit is cut when its first item belongs to an earlier workgroup sa; its
-// pieces are then workgroups sa .. s.
+// pieces are then workgroups sa .. s (a workgroup between them can own none
+// of its items when its range falls between two of them).
 struct MergeJob {
   bool active;  // the unit was cut
   SeqAt q;
@@ -236,7 +259,7 @@ constexpr MergeJob unit_job(const SeqAt& q, const Unit& u, int64_t U, int s, con
   j.q = q;
   j.u = u;
   j.U = U;
-  j.sa = owner(gr, U);
+  j.sa = owner(gr, first_item(U, u.w));
   j.active = j.sa != s;
   j.sa_first = false;
   if (!j.active) return j;
@@ -246,7 +269,7 @@ constexpr MergeJob unit_job(const SeqAt& q, const Unit& u, int64_t U, int s, con
   const SeqAt qa = find(lo_a);
   const Unit ua = locate(lo_a - qa.pre, qa.c);
   const int64_t Ua = qa.pre + ua.start;
-  j.sa_first = Ua == U || (lo_a > Ua + static_cast<int64_t>(ua.w) * qa.c.t_pre && unit_end(qa, ua) == U);
+  j.sa_first = Ua == U || (lo_a > tree_item(Ua, ua.w, qa.c.t_pre) && unit_end(qa, ua) == U);
   return j;
 }
 
