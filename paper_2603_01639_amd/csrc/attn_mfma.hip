@@ -372,9 +372,15 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     k_grp[u] = __builtin_amdgcn_readfirstlane(lp.k_key[u]);
     v_grp[u] = __builtin_amdgcn_readfirstlane(lp.v_key[u]);
   }
+  // LDS byte addresses of the ring and of this wave's 1 KiB block in a slot,
+  // worked out once: a slot's load targets are then scalar adds.
+  const uint32_t ring_lds = lds_addr(&sm.kv[0][0]);
+  uint32_t pos_lds[kKLoads];
+#pragma unroll
+  for (int u = 0; u < kKLoads; ++u) pos_lds[u] = __builtin_amdgcn_readfirstlane(lp.lds_pos[u]);
   auto issue_tile = [&](int t) {
-    const unsigned char* k_s = sm.kv[t % kStages];
-    const unsigned char* v_s = k_s + kKBytes;
+    const uint32_t k_lds = ring_lds + (t % kStages) * kTileBytes;
+    const uint32_t v_lds = k_lds + kKBytes;
     const TileRef tr = tile_ref(t);
     if (paged_uniform && !tr.tree && tr.left >= kKT && (tr.row & (kKT - 1)) == 0) {
       const int64_t in_row = a.kv_rows > kKT ? static_cast<int64_t>(tr.row & (a.kv_rows - 1)) * (HD * 2) : 0;
@@ -388,9 +394,9 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
       for (int u = 0; u < kKLoads; ++u) {
         const int64_t kb = __builtin_amdgcn_readfirstlane(bk[u]);
         const int64_t vb = __builtin_amdgcn_readfirstlane(bv[u]);
-        dma16(lds_addr(k_s + lp.lds_pos[u]), kbase + (((kb * a.Hkv + g) << a.kv_shift) * (HD * 2) + in_row),
+        dma16(k_lds + pos_lds[u], kbase + (((kb * a.Hkv + g) << a.kv_shift) * (HD * 2) + in_row),
               k_poff[u]);
-        dma16(lds_addr(v_s + lp.lds_pos[u]), vbase + (((vb * a.Hkv + g) << a.kv_shift) * (HD * 2) + in_row),
+        dma16(v_lds + pos_lds[u], vbase + (((vb * a.Hkv + g) << a.kv_shift) * (HD * 2) + in_row),
               v_poff[u]);
       }
     } else if (!paged && tr.left >= kKT) {
@@ -398,8 +404,8 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
       const int64_t base = row_byte(tr.row);
 #pragma unroll
       for (int u = 0; u < kKLoads; ++u) {
-        dma16(lds_addr(k_s + lp.lds_pos[u]), kbase + base, k_voff[u]);
-        dma16(lds_addr(v_s + lp.lds_pos[u]), vbase + base, v_voff[u]);
+        dma16(k_lds + pos_lds[u], kbase + base, k_voff[u]);
+        dma16(v_lds + pos_lds[u], vbase + base, v_voff[u]);
       }
     } else {
       // paged rows, or a range's last partial tile (keys past the range's end
@@ -408,8 +414,8 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
       for (int u = 0; u < kKLoads; ++u) {
         const int kk = tr.row + min(lp.k_key[u], tr.left - 1);
         const int vk = tr.row + min(lp.v_key[u], tr.left - 1);
-        dma16(lds_addr(k_s + lp.lds_pos[u]), kbase + row_byte(kk) + k_off[u]);
-        dma16(lds_addr(v_s + lp.lds_pos[u]), vbase + row_byte(vk) + v_off[u]);
+        dma16(k_lds + pos_lds[u], kbase + row_byte(kk) + k_off[u]);
+        dma16(v_lds + pos_lds[u], vbase + row_byte(vk) + v_off[u]);
       }
     }
   };
