@@ -14,25 +14,30 @@
 //     s_{k+1} = sum_v max(P(v) - g_{k+1} Q(v), 0)   (kept if it is 0).
 // So an accept test needs only P(x) and Q(x) and two scalars, each rejection
 // one pass over the vocabulary for s_{k+1}, and the bonus one inverse-CDF pass.
-// The first rejection at any node sets g_2 = 1 exactly, so the masses at g = 0
-// and g = 1 can be taken for every node at once, before the walk.
+// None of g_k, s_k, D_k depends on the uniforms: a node's children are tried in
+// a fixed order, so the residual after its k-th rejection is the same whatever
+// the draws, and its mass can be taken for every node at once, before the
+// walk, one level k per launch (level k needs the total of level k - 1).  The
+// first rejection at any node sets g_2 = 1 exactly.
 //
 //   sample_stats_kernel  grid (vocab chunks of 4096, Nmax, B): per node, the
 //                        chunk's partial of the softmax of logits / T (max and
 //                        sum of exp) and, for nodes with children, the sum of
 //                        its draft row;
-//   sample_mass_kernel   the same grid, nodes with children only: per chunk,
-//                        the residual mass at g = 1 with the walk's own
-//                        parameters (the mass at g = 0 is the chunk's softmax
-//                        partial);
+//   sample_mass_kernel   the same grid, launched for levels k = 1 .. kLevels,
+//                        nodes with at least k children only: per chunk, the
+//                        residual mass after the node's k-th rejection, with
+//                        the walk's own parameters and arithmetic (the mass at
+//                        g = 0 is the chunk's softmax partial);
 //   sample_walk_kernel   one 1024-thread workgroup per sequence walks the tree:
-//                        scalar accept tests; a node's first rejection reads
-//                        its mass from the table, each later one takes a
-//                        block-wide pass; the bonus takes its chunk from the
-//                        table when g is 0 or 1, and otherwise narrows the
-//                        range holding the target mass sixteenfold per level
-//                        (one coalesced segment sum per wave); a wave scan of
-//                        the last 64 tokens or fewer ends the search.
+//                        scalar accept tests; a node's first kLevels rejections
+//                        read their masses from the tables, each later one
+//                        takes a block-wide pass; the bonus takes its chunk from
+//                        a table when its residual is one of them, and
+//                        otherwise narrows the range holding the target mass
+//                        sixteenfold per level (one coalesced segment sum per
+//                        wave); a wave scan of the last 64 tokens or fewer ends
+//                        the search.
 // Element arithmetic is float32, every sum over the vocabulary is finished in
 // double.
 #include "ltd_device.hpp"
@@ -48,6 +53,26 @@ constexpr int kWalkThreads = 1024;
 constexpr int kWalkWaves = kWalkThreads / kWave;
 constexpr int kMaxChunks = LTD_SAMPLING_MAX_CHUNKS;
 static_assert(kMaxChunks <= kWave, "the walk merges one chunk partial a lane");
+constexpr int kLevels = 3;  // rejections per node whose residual masses are tabled
+
+// The residual after a node's rejections so far: P_k = max(P - g Q, 0) / s,
+// and D = the draft mass of the rejected tokens.  The walk and the mass
+// tables advance it with the same operations, so both see bit-identical g.
+struct RejState {
+  double g, s, D;
+};
+// g of the residual after the next rejection.
+__device__ __forceinline__ double next_g(const RejState& st) { return st.g + st.s / (1.0 - st.D); }
+// The rejection of a token with draft probability Qx (counted once even if the
+// token was rejected before), after which the residual at g2 has mass s2 (a
+// residual without mass leaves P as it was).
+__device__ __forceinline__ void reject(RejState& st, double g2, double s2, double Qx, bool repeat) {
+  if (!repeat) st.D += Qx;
+  if (s2 > 0.0) {
+    st.g = g2;
+    st.s = s2;
+  }
+}
 
 // Node j's parent as every kernel here reads it: in [0, j - 1] (the links of
 // a valid tree; malformed ones are clamped, so all kernels agree on the tree).
@@ -215,8 +240,8 @@ __device__ NodeTotals merge_node_stats_of(const NodeStats st, int chunks, int la
   Mf = fmaxf(Mf, lane_xor_f<4>(Mf, lane));
   Mf = fmaxf(Mf, lane_xor_f<2>(Mf, lane));
   Mf = fmaxf(Mf, lane_xor_f<1>(Mf, lane));
-  double zl =
-      m_l != -INFINITY ? static_cast<double>(st.z) * exp(static_cast<double>(m_l - Mf)) : 0.0;
+  // (the chunk's rescale in float: its exponent is a float difference)
+  double zl = m_l != -INFINITY ? static_cast<double>(st.z * __expf(m_l - Mf)) : 0.0;
   double ql = lane < chunks ? static_cast<double>(st.qs) : 0.0;
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) {
@@ -244,7 +269,8 @@ constexpr double kLog2e = 1.4426950408889634;
 __device__ __forceinline__ Residual residual_params(const NodeTotals& nt, float inv_t, double g) {
   Residual r;
   r.a = static_cast<float>(kLog2e * static_cast<double>(inv_t));
-  r.b = static_cast<float>(kLog2e * (static_cast<double>(nt.Mf) + log(nt.Z)));
+  r.b = static_cast<float>(kLog2e * (static_cast<double>(nt.Mf) +
+                                      static_cast<double>(__logf(static_cast<float>(nt.Z)))));
   r.gq = g > 0.0 && nt.QS > 0.0 ? static_cast<float>(g / nt.QS) : 0.f;
   return r;
 }
@@ -326,17 +352,24 @@ __device__ double wave_range_sum(const float* __restrict__ l, const float* __res
   return wave_sum_d(acc, lane);
 }
 
-// Per (node with children, chunk): the residual mass
-// sum_v max(P(v) - Q(v), 0) over the chunk, i.e. at g = 1 (after the node's
-// first rejection, g is exactly 1), with the walk's own parameters and element
-// arithmetic.
+// Per (node with at least `level` children, chunk): the residual mass
+// sum_v max(P(v) - g Q(v), 0) over the chunk after the node's level-th
+// rejection, with the walk's own parameters and element arithmetic.  Level 1
+// is at g = 1; level k replays the node's first k - 1 rejections from the
+// totals of levels 1 .. k - 1 (tables `mass` + (l - 1) * level_stride), the
+// way the walk advances its state.  Other nodes' entries read as 0.
 __global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
     const float* __restrict__ logits, const float* __restrict__ draft_probs,
-    const int32_t* __restrict__ parents, const int32_t* __restrict__ n_nodes, int Nmax, int Voc,
-    float inv_t, const NodeStats* __restrict__ ws, double* __restrict__ mass1,
+    const int32_t* __restrict__ draft_tokens, const int32_t* __restrict__ parents,
+    const int32_t* __restrict__ n_nodes, int Nmax, int Voc, float inv_t,
+    const NodeStats* __restrict__ ws, double* __restrict__ mass, int level, int64_t level_stride,
     const int32_t* status) {
+  static_assert(kStatThreads >= LTD_MAX_NODES, "one thread per node for the child bits");
   __shared__ NodeTotals nt_s;
-  __shared__ int has_child_s;
+  __shared__ uint64_t kids_s[kStatThreads / kWave];
+  __shared__ int tok_s[kLevels];
+  __shared__ int ctok_s[LTD_MAX_NODES];  // tokens of the node's children
+  __shared__ double g_s;
   __shared__ double red_s[kStatThreads / kWave];
   if (halted(status)) return;
   const int chunk = blockIdx.x, i = blockIdx.y, b = blockIdx.z;
@@ -345,20 +378,55 @@ __global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
   const int n = min(max(n_nodes[b], 1), Nmax);
   if (i >= n) return;  // uniform for the block
   const int64_t nb = static_cast<int64_t>(b) * Nmax;
-  if (t == 0) has_child_s = 0;
+  const int64_t row = (nb + i) * Voc;
+  double* out = mass + (level - 1) * level_stride + (nb + i) * chunks + chunk;
+  {  // the node's children as bits, thread j for node j, and their tokens
+    const bool kid = t < n && t > i && link(parents, nb, t) == i;
+    const int tok = min(max(draft_tokens[nb + min(t, n - 1)], 0), Voc - 1);
+    const uint64_t bits = __ballot(kid);
+    if (lane == 0) kids_s[w] = bits;
+    if (kid) ctok_s[t] = tok;
+  }
   if (w == 0) {
     const NodeTotals nt = merge_node_stats(ws + (nb + i) * chunks, chunks, lane);
     if (lane == 0) nt_s = nt;
   }
   __syncthreads();
-  for (int j = t; j < n; j += kStatThreads)
-    if (j > i && link(parents, nb, j) == i) has_child_s = 1;
-  __syncthreads();
-  if (has_child_s == 0) {  // uniform: a leaf never rejects; its entry reads as 0
-    if (t == 0) mass1[(nb + i) * chunks + chunk] = 0.0;
+  int n_kids = 0;
+#pragma unroll
+  for (int word = 0; word < kStatThreads / kWave; ++word) n_kids += __popcll(kids_s[word]);
+  if (n_kids < level) {  // uniform: the node never rejects `level` times
+    if (t == 0) *out = 0.0;
     return;
   }
-  const int64_t row = (nb + i) * Voc;
+  if (t == 0) {  // its first `level` children's tokens, in ascending order
+    int nk = 0;
+    for (int word = 0; word < kStatThreads / kWave && nk < level; ++word) {
+      uint64_t bits = kids_s[word];
+      while (bits != 0 && nk < level) {
+        const int c = word * kWave + __ffsll(static_cast<long long>(bits)) - 1;
+        bits &= bits - 1;
+        tok_s[nk++] = ctok_s[c];
+      }
+    }
+  }
+  __syncthreads();
+  const NodeTotals nt = nt_s;
+  // wave 0's loads for the replay first, then every thread's share of the
+  // chunk's rows, in flight while the residual's g is worked out
+  double prev_mass[kLevels - 1], prev_q[kLevels - 1];
+  if (w == 0) {
+#pragma unroll
+    for (int k = 0; k < kLevels - 1; ++k) {
+      prev_mass[k] = 0.0;
+      prev_q[k] = 0.0;
+      if (k < level - 1) {
+        const double* prev = mass + k * level_stride + (nb + i) * chunks;
+        prev_mass[k] = lane < chunks ? prev[lane] : 0.0;
+        prev_q[k] = static_cast<double>(draft_probs[row + tok_s[k]]);
+      }
+    }
+  }
   const int base = chunk * kChunk;
   float l[kPerThread], q[kPerThread];
 #pragma unroll
@@ -367,19 +435,35 @@ __global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
     l[k] = logits[v];
     q[k] = draft_probs[v];
   }
-  const Residual r1 = residual_params(nt_s, inv_t, 1.0);
-  double d1 = 0.0;
+  if (w == 0) {  // g after `level` rejections: the walk's state, replayed
+    RejState st{0.0, 1.0, 0.0};
+#pragma unroll
+    for (int k = 0; k < kLevels - 1; ++k) {
+      if (k < level - 1) {
+        const double tot = wave_sum_d(prev_mass[k], lane);
+        const double Qx = nt.QS > 0.0 ? prev_q[k] / nt.QS : 0.0;
+        bool repeat = false;
+        for (int j = 0; j < k; ++j) repeat = repeat || tok_s[j] == tok_s[k];
+        const double g2 = next_g(st);
+        reject(st, g2, tot, Qx, repeat);
+      }
+    }
+    if (lane == 0) g_s = next_g(st);
+  }
+  __syncthreads();
+  const Residual r = residual_params(nt, inv_t, g_s);
+  double d = 0.0;
 #pragma unroll
   for (int k = 0; k < kPerThread; ++k)
-    if (base + k * kStatThreads + t < Voc) d1 += static_cast<double>(residual_elem(l[k], q[k], r1));
-  d1 = wave_sum_d(d1, lane);
-  if (lane == 0) red_s[w] = d1;
+    if (base + k * kStatThreads + t < Voc) d += static_cast<double>(residual_elem(l[k], q[k], r));
+  d = wave_sum_d(d, lane);
+  if (lane == 0) red_s[w] = d;
   __syncthreads();
   if (t == 0) {
-    double a1 = 0.0;
+    double a = 0.0;
 #pragma unroll
-    for (int k = 0; k < kStatThreads / kWave; ++k) a1 += red_s[k];
-    mass1[(nb + i) * chunks + chunk] = a1;
+    for (int k = 0; k < kStatThreads / kWave; ++k) a += red_s[k];
+    *out = a;
   }
 }
 
@@ -390,22 +474,72 @@ __device__ __forceinline__ bool child_any(const int32_t* par_s, int n, int u, in
   return __ballot(any) != 0;
 }
 
+// What the walk needs of a node, loaded and merged by one wave (lane c takes
+// chunk c): its softmax maximum, normaliser and draft sum, the totals of its
+// tabled residual masses, and its chunk masses (the softmax's and the
+// tables').  0 for rejections the node cannot have.  The loads and the merge
+// are separate steps, so a wave can have a node's loads in flight while it
+// works on something else.
+constexpr int kNodeVals = 3 + kLevels;
+struct NodeLoads {
+  NodeStats st;
+  double mk[kLevels];
+};
+__device__ __forceinline__ NodeLoads node_loads(const NodeStats* __restrict__ ws,
+                                                const double* __restrict__ mass,
+                                                int64_t level_stride, int64_t nb, int v, int chunks,
+                                                int lane) {
+  NodeLoads r;
+  const int cl = min(lane, chunks - 1);
+  r.st = ws[(nb + v) * chunks + cl];
+#pragma unroll
+  for (int k = 0; k < kLevels; ++k) r.mk[k] = mass[k * level_stride + (nb + v) * chunks + cl];
+  return r;
+}
+__device__ void node_merge(const NodeLoads& ld, const int32_t* par_s, int n, int v, int chunks,
+                           int lane, double* node_out, double (*mass_out)[kLevels + 1]) {
+  const NodeStats st = ld.st;
+  const NodeTotals nt = merge_node_stats_of(st, chunks, lane);
+  const bool kids = child_any(par_s, n, v, lane);
+  const double m0c =
+      st.m != -INFINITY ? static_cast<double>(st.z * __expf(st.m - nt.Mf)) / nt.Z : 0.0;
+  if (lane < chunks) mass_out[lane][0] = m0c;
+  double tot[kLevels];
+#pragma unroll
+  for (int k = 0; k < kLevels; ++k) {
+    const double mc = kids ? ld.mk[k] : 0.0;
+    if (lane < chunks) mass_out[lane][k + 1] = mc;
+    tot[k] = wave_sum_d(lane < chunks ? mc : 0.0, lane);
+  }
+  if (lane == 0) {
+    node_out[0] = nt.Mf;
+    node_out[1] = nt.Z;
+    node_out[2] = nt.QS;
+#pragma unroll
+    for (int k = 0; k < kLevels; ++k) node_out[3 + k] = tot[k];
+  }
+}
+
 __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
     const float* __restrict__ logits, const float* __restrict__ draft_probs,
     const int32_t* __restrict__ draft_tokens, const int32_t* __restrict__ parents,
     const int32_t* __restrict__ n_nodes, const float* __restrict__ uniforms, int Nmax, int Voc,
-    float inv_t, const NodeStats* __restrict__ ws, const double* __restrict__ mass1, int chunks,
-    int32_t* __restrict__ accepted, int32_t* __restrict__ out_tokens,
-    int32_t* __restrict__ n_accepted, const int32_t* status) {
+    float inv_t, const NodeStats* __restrict__ ws, const double* __restrict__ mass,
+    int64_t level_stride, int chunks, int32_t* __restrict__ accepted,
+    int32_t* __restrict__ out_tokens, int32_t* __restrict__ n_accepted, const int32_t* status) {
   __shared__ int32_t par_s[LTD_MAX_NODES];
   __shared__ int32_t tok_s[LTD_MAX_NODES];
   __shared__ uint64_t child_s[LTD_MAX_NODES / kWave];
   __shared__ int32_t path_s[LTD_MAX_NODES];
   __shared__ int32_t removed_s[LTD_MAX_NODES];
+  __shared__ float cl_s[LTD_MAX_NODES], cq_s[LTD_MAX_NODES], cr_s[LTD_MAX_NODES];  // child inputs
   __shared__ double red_s[kWalkWaves];
-  __shared__ double node_s[4];  // M, Z, QS, and the residual mass at g = 1, of the current node
-  __shared__ double2 mass_s[LTD_SAMPLING_MAX_CHUNKS];  // the node's chunk masses at g = 0, 1
+  // The current node's M, Z, QS and tabled residual totals, and its chunk
+  // masses ([0] the softmax's, [k] after its k-th rejection).
+  __shared__ double node_s[1][kNodeVals];
+  __shared__ double mass_s[1][LTD_SAMPLING_MAX_CHUNKS][kLevels + 1];
   __shared__ double target_s;  // the bonus search: mass left to pass in [lo_s, hi_s)
+  __shared__ double seg_s[kWave];  // the bonus search's segment sums
   __shared__ int lo_s, hi_s;
   if (halted(status)) return;
   const int b = blockIdx.x;
@@ -424,44 +558,40 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
   int bonus = 0;
   for (;;) {
     const int64_t row = (nb + u) * Voc;
-    // the node's softmax normaliser and draft sum from the chunk partials,
-    // and its chunk masses at g = 0 (the chunk's softmax mass, from its
-    // partial) and at g = 1 (the mass table; written for nodes with children)
-    if (w == 0) {
-      // both loads first (a leaf's mass entries are 0)
-      const NodeStats st = ws[(nb + u) * chunks + min(lane, chunks - 1)];
-      const double m1_any = mass1[(nb + u) * chunks + min(lane, chunks - 1)];
-      const NodeTotals nt = merge_node_stats_of(st, chunks, lane);
-      const bool kids = child_any(par_s, n, u, lane);
-      const double m1c = kids ? m1_any : 0.0;
-      const double m0c = st.m != -INFINITY
-                             ? static_cast<double>(st.z) *
-                                   exp(static_cast<double>(st.m) - static_cast<double>(nt.Mf)) / nt.Z
-                             : 0.0;
-      if (lane < chunks) mass_s[lane] = make_double2(m0c, m1c);
-      const double m1 = wave_sum_d(lane < chunks ? m1c : 0.0, lane);
-      if (lane == 0) {
-        node_s[0] = nt.Mf;
-        node_s[1] = nt.Z;
-        node_s[2] = nt.QS;
-        node_s[3] = m1;
-      }
+    // Every load first: each child's accept-test inputs (the target logit and
+    // draft probability of its token, its uniform; thread j for node j) and,
+    // in wave 0, the node's stats; then the children as bits of 64-node
+    // words and the node's merged data.
+    const bool is_child = t < n && t < LTD_MAX_NODES && par_s[t] == u && t > u;
+    float cl = 0.f, cq = 0.f, cr = 0.f;
+    if (is_child) {
+      const int x = tok_s[t];
+      cl = logits[row + x];
+      cq = draft_probs[row + x];
+      cr = uniforms[(nb + t) * 2];
     }
-    // the node's children, in ascending order, as bits of 64-node words
+    NodeLoads ld{};
+    if (w == 0) ld = node_loads(ws, mass, level_stride, nb, u, chunks, lane);
     if (t < LTD_MAX_NODES) {
-      const bool is_child = t < n && par_s[t] == u && t > u;
       const uint64_t m = __ballot(is_child);
       if (lane == 0) child_s[w] = m;
+      if (is_child) {
+        cl_s[t] = cl;
+        cq_s[t] = cq;
+        cr_s[t] = cr;
+      }
     }
+    if (w == 0) node_merge(ld, par_s, n, u, chunks, lane, node_s[0], mass_s[0]);
     __syncthreads();
-    const NodeTotals nt{static_cast<float>(node_s[0]), node_s[1], node_s[2]};
+    const NodeTotals nt{static_cast<float>(node_s[0][0]), node_s[0][1], node_s[0][2]};
     const float Mf = nt.Mf;
     const double Z = nt.Z;
     const double QS = nt.QS;
-    const double mass_g1 = node_s[3];
+    const double inv_z = 1.0 / Z;
     Residual res = residual_params(nt, inv_t, 0.0);
 
-    double g = 0.0, s = 1.0, D = 0.0;  // the residual after the rejections so far
+    RejState st{0.0, 1.0, 0.0};  // the residual after the rejections so far
+    int lvl = 0;                 // the mass table holding that residual (-1: none)
     int n_removed = 0;
     int next = -1;
     for (int word = 0; word < LTD_MAX_NODES / kWave && next < 0; ++word) {
@@ -470,45 +600,44 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
         const int c = word * kWave + __ffsll(static_cast<long long>(bits)) - 1;
         bits &= bits - 1;
         const int x = tok_s[c];
-        const double Px =
-            exp(static_cast<double>(logits[row + x] * inv_t) - static_cast<double>(Mf)) / Z;
-        const double Qx = QS > 0.0 ? static_cast<double>(draft_probs[row + x]) / QS : 0.0;
+        // P(x) from a float exponential (its argument is float already; the
+        // walk's hot chain avoids the double exp and divisions)
+        const double Px = static_cast<double>(__expf(cl_s[c] * inv_t - Mf)) * inv_z;
+        const double Qx = QS > 0.0 ? static_cast<double>(cq_s[c]) / QS : 0.0;
         bool removed = false;
         for (int k = 0; k < n_removed; ++k) removed = removed || removed_s[k] == x;
-        const double Pk = fmax(Px - g * Qx, 0.0) / s;
-        const double Qk = removed ? 0.0 : Qx / (1.0 - D);
-        const double r = static_cast<double>(uniforms[(nb + c) * 2]);
-        if (r * Qk < Pk) {
+        // accept when r Q_k(x) < P_k(x), i.e. r Q(x) s < max(P(x) - g Q(x), 0) (1 - D)
+        // (Q_k(x) = 0 for a token rejected before)
+        const double Pres = fmax(Px - st.g * Qx, 0.0);
+        const double r = static_cast<double>(cr_s[c]);
+        const bool accept = removed ? Pres > 0.0 : r * Qx * st.s < Pres * (1.0 - st.D);
+        if (accept) {
           next = c;
           break;
         }
-        // rejected: the next residual's mass.  After the first rejection g is
-        // exactly 1 and the mass table holds it; later ones take one pass
-        // over the vocabulary.
-        const double g2 = g + s / (1.0 - D);
+        // rejected: the next residual's mass, from the tables for the
+        // node's first kLevels rejections, else one pass over the vocabulary
+        const double g2 = next_g(st);
         double s2;
-        if (n_removed == 0) {
-          s2 = mass_g1;
+        if (n_removed < kLevels) {
+          s2 = node_s[0][3 + n_removed];
         } else {
           res = residual_params(nt, inv_t, g2);
           const float part = residual_pass(logits + row, draft_probs + row, Voc, t, res);
           s2 = block_sum(static_cast<double>(part), red_s, lane, w);
         }
-        if (t == 0) removed_s[n_removed] = x;
-        __syncthreads();
-        if (!removed) D += Qx;
+        // (every thread keeps the list, with the same values: no barrier)
+        removed_s[n_removed] = x;
+        reject(st, g2, s2, Qx, removed);
+        if (s2 > 0.0) lvl = n_removed < kLevels ? n_removed + 1 : -1;
         ++n_removed;
-        if (s2 > 0.0) {
-          g = g2;
-          s = s2;
-        }
       }
     }
     if (next >= 0) {
       if (t == 0) path_s[len] = next;
       ++len;
       u = next;
-      __syncthreads();  // node_s / child_s are rewritten for the new node
+      __syncthreads();  // the node's data and child_s are rewritten for the new node
       continue;
     }
 
@@ -519,22 +648,21 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
     // fewer wave 0 takes an inclusive scan and the first token past the
     // target.  Where rounding leaves the target at or past a level's sum, the
     // last segment (token) with mass is taken, as the plain scan would.
-    const bool use_q = g > 0.0;
-    res = residual_params(nt, inv_t, g);
+    const bool use_q = st.g > 0.0;
+    res = residual_params(nt, inv_t, st.g);
     const bool vec = (Voc & 3) == 0 && (reinterpret_cast<uintptr_t>(logits + row) & 15) == 0 &&
                      (reinterpret_cast<uintptr_t>(draft_probs + row) & 15) == 0;
     int lo = 0, hi = Voc;
     bool first = true;  // no level yet: the final scan sets the target itself
-    if (g == 0.0 || g == 1.0) {  // the first level from the mass table's chunks
+    if (lvl >= 0) {  // the first level from a mass table's chunks
       if (t == 0) {
-        const bool g1 = g == 1.0;
         double total = 0.0;
-        for (int c = 0; c < chunks; ++c) total += g1 ? mass_s[c].y : mass_s[c].x;
+        for (int c = 0; c < chunks; ++c) total += mass_s[0][c][lvl];
         const double target = static_cast<double>(uniforms[(nb + u) * 2 + 1]) * total;
         int pick = -1, last = -1;
         double cum = 0.0, before = 0.0, upto_last = 0.0, run = 0.0;
         for (int c = 0; c < chunks && pick < 0; ++c) {
-          const double mc = g1 ? mass_s[c].y : mass_s[c].x;
+          const double mc = mass_s[0][c][lvl];
           if (mc > 0.0) {
             last = c;
             upto_last = run;
@@ -564,6 +692,71 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
     }
     for (; hi - lo > kWave; first = false) {
       const int span = hi - lo;
+      if (vec && span <= kWave * kWave) {
+        // At most 4096 tokens: 64 segments of at most 64 tokens in one step,
+        // 4 per wave, 16 lanes and one float4 per lane and segment; wave 0
+        // scans the 64 sums.
+        const int seg = ((span + 4 * kWave - 1) / (4 * kWave)) * 4;
+        const int k = 4 * w + (lane >> 4);  // this lane's segment
+        const int v = lo + k * seg + 4 * (lane & 15);
+        float part = 0.f;
+        if (v < min(lo + (k + 1) * seg, hi)) {
+          const float4 lv = *reinterpret_cast<const float4*>(logits + row + v);
+          const float4 qv = use_q ? *reinterpret_cast<const float4*>(draft_probs + row + v)
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+          part = residual_elem(lv.x, qv.x, res);
+          part += residual_elem(lv.y, qv.y, res);
+          part += residual_elem(lv.z, qv.z, res);
+          part += residual_elem(lv.w, qv.w, res);
+        }
+        double sum = static_cast<double>(part);
+#pragma unroll
+        for (int d = 8; d >= 1; d >>= 1) {  // over the segment's 16 lanes
+          uint64_t o;
+          const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(sum));
+          switch (d) {
+            case 8: o = lane_xor_u64<8>(bits, lane); break;
+            case 4: o = lane_xor_u64<4>(bits, lane); break;
+            case 2: o = lane_xor_u64<2>(bits, lane); break;
+            default: o = lane_xor_u64<1>(bits, lane);
+          }
+          sum += __longlong_as_double(static_cast<long long>(o));
+        }
+        if (k < kWave && (lane & 15) == 0) seg_s[k] = sum;
+        __syncthreads();
+        if (w == 0) {
+          const double sk = seg_s[lane];
+          double incl = sk;
+#pragma unroll
+          for (int d = 1; d < kWave; d <<= 1) {
+            const double o = __shfl_up(incl, d, kWave);
+            if (lane >= d) incl += o;
+          }
+          const double target = first ? static_cast<double>(uniforms[(nb + u) * 2 + 1]) *
+                                            __shfl(incl, kWave - 1, kWave)
+                                      : target_s;
+          const uint64_t past = __ballot(incl > target && sk > 0.0);
+          const uint64_t withm = __ballot(sk > 0.0);
+          // (past the end by rounding: the last segment with mass; none: token 0)
+          const int pick = past != 0 ? __ffsll(static_cast<long long>(past)) - 1
+                                     : (withm != 0 ? 63 - __clzll(static_cast<long long>(withm)) : -1);
+          const double before = pick >= 0 ? __shfl(incl - sk, pick, kWave) : 0.0;
+          if (lane == 0) {
+            if (pick < 0) {
+              lo_s = 0;
+              hi_s = 0;
+            } else {
+              lo_s = min(lo + pick * seg, hi);
+              hi_s = min(lo + (pick + 1) * seg, hi);
+            }
+            target_s = target - before;
+          }
+        }
+        __syncthreads();
+        lo = lo_s;
+        hi = hi_s;
+        continue;
+      }
       const int seg = vec ? ((span + 4 * kWalkWaves - 1) / (4 * kWalkWaves)) * 4
                           : (span + kWalkWaves - 1) / kWalkWaves;
       const int s_lo = min(lo + w * seg, hi), s_hi = min(s_lo + seg, hi);
@@ -650,7 +843,7 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
 int sampling_chunks(int Voc) { return (Voc + kChunk - 1) / kChunk; }
 
 size_t sampling_workspace_bytes(int B, int Nmax, int Voc) {
-  return (sizeof(NodeStats) + sizeof(double)) * static_cast<size_t>(B) * Nmax *
+  return (sizeof(NodeStats) + kLevels * sizeof(double)) * static_cast<size_t>(B) * Nmax *
          sampling_chunks(Voc);
 }
 
@@ -661,16 +854,20 @@ hipError_t launch_sampling(const float* logits, const float* draft_probs,
                            int32_t* out_tokens, int32_t* n_accepted, void* workspace,
                            const int32_t* status, hipStream_t stream) {
   const int chunks = sampling_chunks(Voc);
+  const int64_t level_stride = static_cast<int64_t>(B) * Nmax * chunks;  // doubles per table
   auto* ws = static_cast<NodeStats*>(workspace);
-  auto* mass1 = reinterpret_cast<double*>(ws + static_cast<size_t>(B) * Nmax * chunks);
+  auto* mass = reinterpret_cast<double*>(ws + level_stride);
   const float inv_t = 1.0f / temperature;
   hipLaunchKernelGGL(sample_stats_kernel, dim3(chunks, Nmax, B), dim3(kStatThreads), 0, stream,
                      logits, draft_probs, parents, n_nodes, Nmax, Voc, inv_t, ws, status);
-  hipLaunchKernelGGL(sample_mass_kernel, dim3(chunks, Nmax, B), dim3(kStatThreads), 0, stream,
-                     logits, draft_probs, parents, n_nodes, Nmax, Voc, inv_t, ws, mass1, status);
+  // level k needs the totals of level k - 1: one launch per level
+  for (int level = 1; level <= kLevels; ++level)
+    hipLaunchKernelGGL(sample_mass_kernel, dim3(chunks, Nmax, B), dim3(kStatThreads), 0, stream,
+                       logits, draft_probs, draft_tokens, parents, n_nodes, Nmax, Voc, inv_t, ws,
+                       mass, level, level_stride, status);
   hipLaunchKernelGGL(sample_walk_kernel, dim3(B), dim3(kWalkThreads), 0, stream, logits,
                      draft_probs, draft_tokens, parents, n_nodes, uniforms, Nmax, Voc, inv_t, ws,
-                     mass1, chunks, accepted_nodes, out_tokens, n_accepted, status);
+                     mass, level_stride, chunks, accepted_nodes, out_tokens, n_accepted, status);
   return hipGetLastError();
 }
 
