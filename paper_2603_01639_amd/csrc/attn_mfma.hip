@@ -82,6 +82,7 @@ constexpr int kKLoads = kLoadsPerTile / 2;  // K (and V) chunks per lane per til
 // probabilities stay below 2^kLazyMax, exact in fp32 and well inside bf16
 // range, and the O/l rescale runs only when the max really moves.
 constexpr float kLazyMax = 8.f;
+constexpr float kNoMax = -__FLT_MAX__;  // running max before any key (raw score units)
 constexpr int kStages = 4;                // K/V tiles in the LDS ring
 constexpr int kMaxSplitTiles = 32;        // split plan: longest split in key tiles
 constexpr int kMaxMergeSplits = 1024;     // split plan: splits the merge takes at most
@@ -149,6 +150,18 @@ __host__ __device__ __forceinline__ int n_splits_of(int P, int n, int split_keys
     if (last_tiles + (n + kKT - 1) / kKT > split_keys / kKT) return pre + 1;
   }
   return pre;
+}
+
+// The larger of x in lanes l and l ^ 32, in every lane: the swap of x with
+// itself leaves the lower half's values in both halves of the first result and
+// the upper half's in both halves of the second.
+__device__ __forceinline__ float max_xor32(float x) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  // (the halves are copied out first: hipcc folds a bit-cast of element 1 of
+  // the result to element 0)
+  const uint32_t lo = r[0], hi = r[1];
+  return __builtin_elementwise_maximum(__builtin_bit_cast(float, lo), __builtin_bit_cast(float, hi));
 }
 
 __device__ __forceinline__ lds_void* as_lds(const void* p) { return (lds_void*)(p); }
@@ -511,7 +524,10 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   }
 
   // ---- online softmax state (raw score units) and O^T accumulators
-  float m_run = -INFINITY, l_run = 0.f;
+  // m starts at the most negative finite float: the first key that is not
+  // masked moves it (a score at that very value gets weight 2^0), and no step
+  // needs a case for -inf.
+  float m_run = kNoMax, l_run = 0.f;
   f32x16 o_acc[HD / 32];
 #pragma unroll
   for (int db = 0; db < HD / 32; ++db) o_acc[db] = f32x16{};
@@ -576,20 +592,19 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
       }
     }
   };
-  float m_new = -INFINITY, psum = 0.f;
+  float m_new = kNoMax, psum = 0.f;
   auto exponentials = [&](f32x16(&s)[2], bf16x8(&pf)[2][2]) {
     // IEEE maximum (NaN-propagating) needs no operand canonicalisation and
     // maps to three-input v_maximum3_f32.
-    float tmax = -INFINITY;
+    float tmax = __builtin_elementwise_maximum(s[0][0], s[0][1]);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; r += 2)
-        tmax = __builtin_elementwise_maximum(tmax, __builtin_elementwise_maximum(s[kb][r], s[kb][r + 1]));
-    tmax = __builtin_elementwise_maximum(tmax, xor32(tmax));
+    for (int r = 2; r < 32; r += 2)
+      tmax = __builtin_elementwise_maximum(__builtin_elementwise_maximum(tmax, s[r >> 4][r & 15]),
+                                           s[r >> 4][(r & 15) + 1]);
+    tmax = max_xor32(tmax);
     // (scale > 0, so the lazy test can run on raw scores)
     m_new = tmax > m_run + a.lazy_gap ? tmax : m_run;
-    const float neg = (m_new == -INFINITY) ? 0.f : -m_new * c;
+    const float neg = -m_new * c;
     // The row sum adds the rounded bf16 probabilities, two per
     // v_dot2_f32_bf16 with ones: the very weights P.V multiplies.
     const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
@@ -616,7 +631,7 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   };
   auto finish_softmax = [&]() {
     if (__builtin_amdgcn_ballot_w64(m_new != m_run) != 0) {
-      const float alpha = (m_new == -INFINITY) ? 1.f : exp2_fast((m_run - m_new) * c);
+      const float alpha = exp2_fast((m_run - m_new) * c);
       l_run *= alpha;
 #pragma unroll
       for (int db = 0; db < HD / 32; ++db) o_acc[db] *= alpha;
@@ -718,7 +733,7 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   {
     const float lsum = l_run + xor32(l_run);
     if (!final_out && qvalid && h == 0) {
-      f32x2 ml = {m_run * c, lsum};
+      f32x2 ml = {lsum > 0.f ? m_run * c : -INFINITY, lsum};
       __builtin_nontemporal_store(ml, reinterpret_cast<f32x2*>(a.ws_ml + (part + qrow_idx) * 2));
     }
     const float inv = lsum > 0.f ? 1.f / lsum : 0.f;

@@ -273,3 +273,31 @@ def test_head_dim_64_batches(block_size):
     trees = [W.tree_uniform_parent(rng, n) for n in (17, 90)]
     _full_step(_custom(trees, [1000, 3000], Hq=4, Hkv=4, d=64, block_size=block_size,
                        seed=641 + block_size, label=f"d64 G=1 block={block_size}"))
+
+
+def _rescaled(b, q_scale, k_fn, label):
+    """b with Q multiplied by q_scale (q_scale 0: every element -40) and K
+    replaced by k_fn(K), re-rounded to bf16: scores far from the usual range."""
+    import dataclasses
+    qf = W.bf16_bits_to_f32(b.q)
+    qf = np.full_like(qf, np.float32(-40.0)) if q_scale == 0.0 else qf * np.float32(q_scale)
+    q = W.f32_to_bf16_bits(qf)
+    k = W.f32_to_bf16_bits(k_fn(W.bf16_bits_to_f32(b.k_cache)).astype(np.float32))
+    return dataclasses.replace(b, q=q, k_cache=k, label=label)
+
+
+@pytest.mark.parametrize("paged", [False, True])
+def test_extreme_score_magnitudes(paged):
+    """Scores near -2e5 (every key far below zero; the scaled scores stay
+    within the 1e5 or so where an fp32 exponent argument keeps an absolute
+    error under 1e-2) and of std ~ 300 (the reference max moves over many
+    tiles): both work plans, against the fp64 oracle."""
+    rng = np.random.default_rng(21)
+    trees = [W.tree_uniform_parent(rng, n) for n in (40, 7, 64)]
+    bs = 16 if paged else 0
+    base = _custom(trees, [1500, 300, 2200], Hq=8, Hkv=2, block_size=bs, seed=21, label="extreme")
+    one = _custom(trees[:1], [2900], Hq=8, Hkv=2, block_size=bs, seed=22, label="extreme B=1")
+    for b in (base, one):
+        # q = -40 elementwise, k in [0.5, 1.5] * 40: every score near -2e5
+        _full_step(_rescaled(b, 0.0, lambda k: 40.0 * (1.0 + 0.5 * np.tanh(k)), b.label + " -2e5"))
+        _full_step(_rescaled(b, 5.0, lambda k: 5.0 * k, b.label + " std 300"))
