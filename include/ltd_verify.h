@@ -173,7 +173,7 @@ int ltd_tree_accept(const float* logits, const int32_t* draft_tokens, const int3
  * nothing and frees nothing.
  *
  * Limits: ltd_tree_accept_workspace_size(B, Nmax, Voc) must not exceed
- * ltd_tree_accept_noalloc_max_bytes() (B * Nmax * ceil(Voc / 8192) * 8 bytes;
+ * ltd_tree_accept_noalloc_max_bytes() (B * Nmax * ceil(Voc / 16384) * 8 bytes;
  * e.g. B = 16, Nmax = 256 and Voc = 262144 use 1 MiB), else LTD_EWORKSPACE and
  * nothing is launched.  LTD_EHIP if the scratch's device address cannot be
  * looked up on the current GPU.

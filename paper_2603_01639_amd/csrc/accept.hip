@@ -29,7 +29,7 @@ namespace ltd {
 namespace {
 
 constexpr int kArgmaxThreads = 256;
-constexpr int kChunk = 8192;                                // logits per workgroup (32 KiB)
+constexpr int kChunk = 16384;                               // logits per workgroup (64 KiB)
 constexpr int kVecPerThread = kChunk / 4 / kArgmaxThreads;  // 16-byte loads per thread
 constexpr int kScanThreads = LTD_MAX_NODES;                 // one thread per node
 constexpr int kKeysPerRound = 8;                            // key loads in flight per thread

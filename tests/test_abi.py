@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_version_and_workspace_queries():
     assert "gfx950" in ltd.version()
-    assert ltd.accept_workspace_size(1, 60, 128256) == 1 * 60 * 16 * 8
+    assert ltd.accept_workspace_size(1, 60, 128256) == 1 * 60 * 8 * 8
     assert ltd.accept_workspace_size(1, 300, 10) == 0  # Nmax above the node limit
     assert ltd.attn_workspace_size(1, 60, 32, 8, 96, 2048, ltd.DTYPE_BF16) == 0  # unsupported d
     assert ltd.attn_grid(1, 60, 32, 8, 128, 2048, ltd.DTYPE_BF16, 0) == -1  # kv_rows < 1
