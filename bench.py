@@ -411,7 +411,7 @@ def main():
 
 
 EXTRA_WORKLOADS = ([("c2", None), ("c3", None)] + [("c4", n) for n in (8, 16, 32, 64, 128, 256)]
-                   + [("c2_d64", None)])
+                   + [("c2_d64", None), ("c5_tp8", None)])
 
 
 def workload_key(name, c4_n=None):
@@ -436,6 +436,8 @@ def attention_by_workload(ltd, torch, to_dev, args, graph_of, timed, stream):
             b = W.config3_long(0, with_logits=False)
         elif name == "c2_d64":
             b = W.config2_d64(0, with_logits=False)
+        elif name == "c5_tp8":
+            b = W.config5_tp_share(0, 8)
         else:
             b = W.config4_sweep(n, min(6, n), with_logits=False)
         attn_bytes, _, flops = algorithmic_bytes(b)

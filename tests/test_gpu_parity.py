@@ -60,6 +60,13 @@ def test_config5_paged_batch(rep):
     _full_step(W.config5_paged(rep))
 
 
+@pytest.mark.parametrize("rep", range(3))
+def test_config5_tp8_share(rep):
+    """One GPU's share of c5 under 8-way tensor parallelism (one kv head, 8 q
+    heads per sequence): every node and head against the oracle."""
+    _full_step(W.config5_tp_share(rep, 8))
+
+
 def test_config5_deterministic():
     """Two runs of the batched paged step give bit-identical outputs: the
     split merge order is fixed, whatever order the workgroups finish in."""

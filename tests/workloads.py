@@ -418,6 +418,26 @@ def config5_paged(rep: int = 0, with_logits: bool = True, B: int = 16) -> Verify
                       with_logits=with_logits, label="70B bf16 paged B16")
 
 
+def config5_tp_share(rep: int = 0, tp: int = 8) -> VerifyBatch:
+    """One GPU's share of the c5 batch under tp-way tensor parallelism over
+    the kv heads: the same sequences, prefixes, trees and 16-token paged
+    layout as config5_paged, with 64/tp query and 8/tp kv heads.  Attention
+    only: acceptance needs the whole vocabulary, which a vocabulary-sharded LM
+    head gathers first."""
+    rng = rng_for(config_seed(5, rep))
+    B = 16
+    prefix = [int(rng.integers(1024, 8193)) for _ in range(B)]
+    ns = [int(rng.integers(16, 129)) for _ in range(B)]
+    trees, toks = [], []
+    for b in range(B):
+        t = tree_eagle(rng, ns[b], 6, 10, 128256)
+        trees.append(t.parents)
+        toks.append(t.tokens)
+    return make_batch(rng, dtype=DTYPE_BF16, Hq=64 // tp, Hkv=8 // tp, d=128, prefix=prefix,
+                      trees=trees, tokens=toks, Voc=128256, p_match=0.7, Nmax=max(ns),
+                      block_size=16, with_logits=False, label=f"70B bf16 paged B16, TP{tp} share")
+
+
 # ------------------------------------------------------ candidate selection
 
 MAX_POOL = 1024  # candidate pools up to 1 + W + (D-2) W^2 = 1011 (W = 10, D = 12)
