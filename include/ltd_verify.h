@@ -102,7 +102,11 @@ extern "C" {
  * g = h / (Hq / Hkv)):
  *     out[b][i][h] = softmax_t(scale * <q[b][i][h], K[b][g][t]>) . V[b][g][t]
  * over the visible rows t = {0, ..., P_b - 1} u {P_b + j : j on the root path of
- * node i, i included}.  Accumulation is fp32; out has the input dtype.
+ * node i, i included}.  Accumulation is fp32; out has the input dtype.  On
+ * the bf16 path the exponent of each weight is formed in fp32 as
+ * s*c - m*c (c = scale * log2(e), m a running row maximum), exact to about
+ * |m*c| * 2^-24: scaled scores up to ~1e5 in magnitude keep the bf16 output
+ * accuracy (max-abs error ~1e-2 against exact arithmetic).
  *
  *   q           [B][Nmax][Hq][d] (dtype): the tree nodes' queries (position
  *               encoding already applied by the caller).
