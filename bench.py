@@ -5,7 +5,7 @@ sequences with 70B-shaped attention (64 q / 8 kv heads, head_dim 128, bf16),
 prefixes of 1024-8192 tokens in a paged cache of 16-token blocks, and draft
 trees of 16-128 nodes.
 
-    python bench.py [--steps K] [--warmup W] [--workload c2|c3|c4|c5] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload c1|c2|c3|c4|c5] [--no-cpu-baseline]
 
 Prints ONE JSON line.  `value` is microseconds per verify step (lower is
 better): K back-to-back steps are captured into one HIP graph, as a serving
@@ -61,7 +61,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="c5", choices=["c2", "c3", "c4", "c5"])
+    ap.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--c4-n", type=int, default=64)
     ap.add_argument("--c4-depth", type=int, default=6)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -75,7 +75,11 @@ def parse():
 
 def make_workload(args):
     import workloads as W
-    if args.workload == "c2":
+    if args.workload == "c1":
+        b = W.config1_tiny_f32(0)
+        desc = ("tiny fp32 tree verify: batch 1, 8 q / 8 kv heads, head_dim 64, prefix 128, "
+                "16-node uniform-parent tree, vocab 1000, greedy (launch-bound correctness case)")
+    elif args.workload == "c2":
         b = W.config2_8b(0)
         desc = ("Llama-3-8B-shaped bf16 tree verify: batch 1, 32 q / 8 kv heads, head_dim 128, "
                 "prefix 2048, 60-node Eagle tree (depth 6, top-10), vocab 128256, greedy")
@@ -97,7 +101,7 @@ def make_workload(args):
 def select_workload(name):
     """Candidate pools shaped like each verify workload's trees."""
     import workloads as W
-    return {"c2": W.select_8b, "c3": W.select_8b, "c4": W.select_deep,
+    return {"c1": W.select_8b, "c2": W.select_8b, "c3": W.select_8b, "c4": W.select_deep,
             "c5": W.select_batch16}[name](0)
 
 

@@ -1,5 +1,5 @@
 // Launch planning and dispatch for tree attention: bf16 (head_dim 128 or 64)
-// runs on the MFMA kernels, fp32 on the row-wise VALU kernel.
+// runs on the MFMA kernels, fp32 on the tiled VALU kernel (attn_rowwise.hip).
 #include "ltd_device.hpp"
 #include "ltd_launch.hpp"
 
