@@ -125,7 +125,7 @@ extern "C" {
  *               attention); anything else is LTD_EINVAL.
  *   workspace   device scratch of at least ltd_tree_verify_attn_workspace_size()
  *               bytes for the same (B, Nmax, Hq, Hkv, d, max_prefix, dtype) (that
- *               size covers every cache layout; it is 0 on the row-wise path,
+ *               size covers every cache layout; it is 0 on the fp32 path,
  *               and workspace may then be NULL); it holds the partial results
  *               of units cut between workgroups, needs no initialisation and
  *               is garbage afterwards.
@@ -260,7 +260,7 @@ int ltd_kv_compact(void* k_cache, void* v_cache, const int32_t* block_table,
  * its (sequence, kv head, row tile) units' key tiles end to end and gives each
  * of that many workgroups (a power of two) an equal share; a single sequence
  * cuts each unit into KV splits.  Units cut between workgroups are merged by a
- * second kernel.  0 when the call runs on the row-wise kernel instead (fp32),
+ * second kernel.  0 when the call runs on the fp32 vector kernel instead,
  * -1 on bad args.
  * Introspection for tests and benchmarks. */
 int ltd_tree_verify_attn_grid(int B, int Nmax, int Hq, int Hkv, int d, int max_prefix, int dtype,
