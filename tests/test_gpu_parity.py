@@ -308,3 +308,23 @@ def test_extreme_score_magnitudes(paged):
         # q = -40 elementwise, k in [0.5, 1.5] * 40: every score near -2e5
         _full_step(_rescaled(b, 0.0, lambda k: 40.0 * (1.0 + 0.5 * np.tanh(k)), b.label + " -2e5"))
         _full_step(_rescaled(b, 5.0, lambda k: 5.0 * k, b.label + " std 300"))
+
+
+@pytest.mark.parametrize("paged", [False, True])
+def test_long_prefix_65536(paged):
+    """One sequence with a 65536-token prefix (the split plan at its longest
+    splits and most pieces), contiguous and in 16-token blocks."""
+    rng = np.random.default_rng(65536)
+    trees = [W.tree_uniform_parent(rng, 48)]
+    _full_step(_custom(trees, [65536], Hq=16, Hkv=2, block_size=16 if paged else 0, seed=65,
+                       label=f"P=65536 paged={paged}"))
+
+
+def test_many_sequences():
+    """64 sequences of mixed prefixes and tree sizes (the stream plan with
+    many short units), in 16-token blocks."""
+    rng = np.random.default_rng(64)
+    ns = [int(rng.integers(1, 40)) for _ in range(64)]
+    ps = [int(rng.integers(0, 1500)) for _ in range(64)]
+    trees = [W.tree_uniform_parent(rng, n) if n > 1 else np.array([-1], np.int32) for n in ns]
+    _full_step(_custom(trees, ps, Hq=8, Hkv=2, block_size=16, seed=64, label="B=64"))
