@@ -23,7 +23,57 @@ constexpr int kVecThreads = kVecWaves * kWave;
 constexpr int kMaxD = 128;
 constexpr int kPieces = kTileKeys * kMaxD / 4 / kVecThreads;  // 16-byte pieces a thread loads
 
-template <typename T>
+// Wave-wide reductions without the LDS crossbar: within each 16-lane row by
+// DPP (quad swaps, then the half-row and row mirrors: every lane ends with its
+// row's total), then across rows with v_permlane16_swap and
+// v_permlane32_swap of the value with itself (their two results hold the
+// other row, or half, in every lane).
+template <int kCtrl>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), kCtrl,
+                                                               0xF, 0xF, false));
+}
+template <class Op>
+__device__ __forceinline__ float wave_reduce(float v, Op op) {
+  v = op(v, dpp<0xB1>(v));   // quad_perm [1, 0, 3, 2]
+  v = op(v, dpp<0x4E>(v));   // quad_perm [2, 3, 0, 1]
+  v = op(v, dpp<0x141>(v));  // row_half_mirror
+  v = op(v, dpp<0x140>(v));  // row_mirror
+  uint32_t u = __builtin_bit_cast(uint32_t, v);
+  const auto r16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  // (the halves are copied out first: hipcc folds a bit-cast of element 1 of
+  // the result to element 0)
+  const uint32_t a = r16[0], b = r16[1];
+  v = op(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+  u = __builtin_bit_cast(uint32_t, v);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const uint32_t c = r32[0], e = r32[1];
+  return op(__builtin_bit_cast(float, c), __builtin_bit_cast(float, e));
+}
+__device__ __forceinline__ float wave_max_dpp(float v) {
+  return wave_reduce(v, [](float x, float y) { return fmaxf(x, y); });
+}
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+  return wave_reduce(v, [](float x, float y) { return x + y; });
+}
+
+// Four consecutive elements of a cache row as floats (16-byte loads when the
+// row data is float and 16-byte aligned).
+template <typename T, bool kVec>
+__device__ __forceinline__ void load4(const T* p, int64_t i, float (&x)[4]) {
+  if constexpr (kVec) {
+    const float4 v = *reinterpret_cast<const float4*>(p + i);
+    x[0] = v.x;
+    x[1] = v.y;
+    x[2] = v.z;
+    x[3] = v.w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = load_f32(p, i + e);
+  }
+}
+
+template <typename T, bool kVec>
 __global__ void __launch_bounds__(kVecThreads) attn_vector_kernel(
     const T* __restrict__ q, const T* __restrict__ k_cache, const T* __restrict__ v_cache,
     const int32_t* __restrict__ block_table, const int32_t* __restrict__ prefix_len,
@@ -76,11 +126,8 @@ __global__ void __launch_bounds__(kVecThreads) attn_vector_kernel(
           const int kt = base + r;
           const int row = kt < P ? kt : P + path_s[kt - P];
           const int64_t off = cache_row(block_table, b, g, row, Hkv, d, kv_rows, max_blocks) + c;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            kr4[j][e] = load_f32(k_cache, off + e);
-            vr4[j][e] = load_f32(v_cache, off + e);
-          }
+          load4<T, kVec>(k_cache, off, kr4[j]);
+          load4<T, kVec>(v_cache, off, vr4[j]);
         }
       }
     };
@@ -121,10 +168,10 @@ __global__ void __launch_bounds__(kVecThreads) attn_vector_kernel(
         }
         if (lane < cnt) s = (d4[0] + d4[1]) + (d4[2] + d4[3]);
       }
-      const float m_new = fmaxf(m, wave_max(s));
+      const float m_new = fmaxf(m, wave_max_dpp(s));
       const float p = lane < cnt ? expf(s - m_new) : 0.f;
       const float alpha = expf(m - m_new);
-      l = l * alpha + wave_sum(p);
+      l = l * alpha + wave_sum_dpp(p);
       acc0 *= alpha;
       acc1 *= alpha;
       m = m_new;
@@ -165,13 +212,18 @@ hipError_t launch_attn_rowwise(const AttnShape& s, const void* q, const void* k_
                                const int32_t* status, hipStream_t stream) {
   const dim3 grid(s.Nmax, s.Hkv, s.B);
   if (s.dtype == LTD_DTYPE_F32) {
-    hipLaunchKernelGGL(attn_vector_kernel<float>, grid, dim3(kVecThreads), 0, stream,
+    // 16-byte loads when both caches are 16-byte aligned (every row and piece
+    // offset is a multiple of 4 elements)
+    const bool vec = (reinterpret_cast<uintptr_t>(k_cache) % 16) == 0 &&
+                     (reinterpret_cast<uintptr_t>(v_cache) % 16) == 0;
+    auto kern = vec ? attn_vector_kernel<float, true> : attn_vector_kernel<float, false>;
+    hipLaunchKernelGGL(kern, grid, dim3(kVecThreads), 0, stream,
                        static_cast<const float*>(q), static_cast<const float*>(k_cache),
                        static_cast<const float*>(v_cache), block_table, prefix_len, parents,
                        n_nodes, static_cast<float*>(out), s.Nmax, s.Hq, s.Hkv, s.d, s.kv_rows,
                        s.max_blocks, scale, status);
   } else {
-    hipLaunchKernelGGL(attn_vector_kernel<uint16_t>, grid, dim3(kVecThreads), 0, stream,
+    hipLaunchKernelGGL((attn_vector_kernel<uint16_t, false>), grid, dim3(kVecThreads), 0, stream,
                        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_cache),
                        static_cast<const uint16_t*>(v_cache), block_table, prefix_len, parents,
                        n_nodes, static_cast<uint16_t*>(out), s.Nmax, s.Hq, s.Hkv, s.d,
