@@ -124,6 +124,7 @@ def test_padded_rows_untouched_and_mixed_batch():
 
 
 @pytest.mark.parametrize("dtype,d,G", [(W.DTYPE_F32, 128, 4), (W.DTYPE_F32, 64, 1),
+                                       (W.DTYPE_F32, 64, 8), (W.DTYPE_F32, 128, 6),
                                        (W.DTYPE_BF16, 64, 8), (W.DTYPE_BF16, 128, 1)])
 def test_head_dims_dtypes_and_groups(dtype, d, G):
     rng = np.random.default_rng(d + G)
@@ -328,3 +329,22 @@ def test_many_sequences():
     ps = [int(rng.integers(0, 1500)) for _ in range(64)]
     trees = [W.tree_uniform_parent(rng, n) if n > 1 else np.array([-1], np.int32) for n in ns]
     _full_step(_custom(trees, ps, Hq=8, Hkv=2, block_size=16, seed=64, label="B=64"))
+
+
+def test_fp32_unaligned_caches():
+    """fp32 K/V caches whose base addresses are 4 but not 16 bytes aligned
+    (the kernel's element-wise load path), against the oracle."""
+    import torch
+    rng = np.random.default_rng(44)
+    trees = [W.tree_uniform_parent(rng, n) for n in (23, 5)]
+    b = _custom(trees, [200, 77], Hq=8, Hkv=2, d=64, dtype=W.DTYPE_F32, seed=44, label="fp32 unaligned")
+    dev = U.upload(b)
+    for name in ("k", "v"):
+        t = getattr(dev, name)
+        buf = torch.empty(t.numel() + 1, dtype=t.dtype, device="cuda")
+        view = buf[1:].view(t.shape)
+        view.copy_(t)
+        assert view.data_ptr() % 16 != 0
+        setattr(dev, name, view)
+    got = U.gpu_attention(b, dev)
+    U.compare_attention(b, got, U.oracle_attention(b))
