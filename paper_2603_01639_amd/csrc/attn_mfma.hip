@@ -815,13 +815,14 @@ __device__ __forceinline__ int64_t readlane_i64(int64_t v, int l) {
 
 // The call's sequence table on the axis, one sequence per lane: lane l of a
 // wave holds sequence l (its clamped prefix length and node count, first axis
-// position and axis length), and every lane holds the total length C.  With
+// position and axis length), and every lane holds the total length C.  (The
+// kernels never need a unit's index among the call's units, so SeqAt::ubase
+// is left 0.)  With
 // more than 64 sequences the lanes hold the first 64 and positions past them
 // are found by rescanning the table (axis_find).
 struct Axis {
   int P, n;
   int64_t start, len;
-  int ubase;  // index of this lane's sequence's first unit
   int64_t C;
 };
 
@@ -847,29 +848,23 @@ __device__ Axis axis_load(const MfmaArgs& a) {
     ax.P = P;
     ax.n = n;
     ax.start = 0;
-    ax.ubase = 0;
     ax.len = lane == 0 ? a.Hkv * c.per_head : 0;
     ax.C = a.Hkv * c.per_head;
     return ax;
   }
   int64_t base = 0;
-  int ubase = 0;
   for (int c0 = 0; c0 < a.B; c0 += kWave) {
     int P, n;
     const plan::SeqCost c = lane_cost(a, c0 + lane, &P, &n);
     const int64_t len = c0 + lane < a.B ? a.Hkv * c.per_head : 0;
     const int64_t x = wave_scan_i64(len);
-    const int nu = c0 + lane < a.B ? a.Hkv * c.rt : 0;
-    const int xu = static_cast<int>(wave_scan_i64(nu));
     if (c0 == 0) {
       ax.P = P;
       ax.n = n;
       ax.start = x - len;
       ax.len = len;
-      ax.ubase = xu - nu;
     }
     base += readlane_i64(x, kWave - 1);
-    ubase += __builtin_amdgcn_readlane(xu, kWave - 1);
   }
   ax.C = base;
   return ax;
@@ -885,22 +880,17 @@ __device__ plan::SeqAt axis_find(const MfmaArgs& a, const Axis& ax, int64_t p) {
     r.P = __builtin_amdgcn_readlane(ax.P, l);
     r.n = __builtin_amdgcn_readlane(ax.n, l);
     r.pre = readlane_i64(ax.start, l);
-    r.ubase = __builtin_amdgcn_readlane(ax.ubase, l);
     r.c = plan::seq_cost(r.P, r.n, a.G);
     return r;
   }
   // past the first 64 sequences: rescan the table from the second chunk on
   const int lane = __lane_id();
   int64_t base = readlane_i64(ax.start + ax.len, kWave - 1);
-  int ubase = __builtin_amdgcn_readlane(ax.ubase, kWave - 1) +
-              __builtin_amdgcn_readlane(a.Hkv * plan::seq_cost(ax.P, ax.n, a.G).rt, kWave - 1);
   for (int c0 = kWave; c0 < a.B; c0 += kWave) {
     int P, n;
     const plan::SeqCost c = lane_cost(a, c0 + lane, &P, &n);
     const int64_t len = c0 + lane < a.B ? a.Hkv * c.per_head : 0;
     const int64_t x = wave_scan_i64(len);
-    const int nu = c0 + lane < a.B ? a.Hkv * c.rt : 0;
-    const int xu = static_cast<int>(wave_scan_i64(nu));
     const int64_t start = base + x - len;
     const uint64_t h = __ballot(len > 0 && start <= p && p < start + len);
     if (h != 0) {
@@ -909,12 +899,10 @@ __device__ plan::SeqAt axis_find(const MfmaArgs& a, const Axis& ax, int64_t p) {
       r.P = __builtin_amdgcn_readlane(P, l);
       r.n = __builtin_amdgcn_readlane(n, l);
       r.pre = readlane_i64(start, l);
-      r.ubase = ubase + __builtin_amdgcn_readlane(xu - nu, l);
       r.c = plan::seq_cost(r.P, r.n, a.G);
       return r;
     }
     base += readlane_i64(x, kWave - 1);
-    ubase += __builtin_amdgcn_readlane(xu, kWave - 1);
   }
   return r;  // not reached for p < C
 }
