@@ -101,7 +101,8 @@ struct MfmaArgs {
   const int32_t* n_nodes;
   uint16_t* ws_o;  // [2W][256][128] bf16: a piece's O / l (slot 2s or 2s + 1)
   float* ws_ml;    // [2W][256][2]: max (log2 units), sum l
-  MergeDesc* ws_desc;  // [W]: entry s, the unit cut at workgroup s's start (if any)
+  MergeDesc* ws_desc;  // [units]: each unit's merge (after a 64-byte header: the unit count)
+  int max_units;       // units the launch can have at most (table entries)
   uint16_t* out;
   const int32_t* status;
   int B, Nmax, Hq, Hkv, G, kv_rows, max_blocks, max_prefix;
@@ -815,15 +816,15 @@ __device__ __forceinline__ int64_t readlane_i64(int64_t v, int l) {
 
 // The call's sequence table on the axis, one sequence per lane: lane l of a
 // wave holds sequence l (its clamped prefix length and node count, first axis
-// position and axis length), and every lane holds the total length C.  (The
-// kernels never need a unit's index among the call's units, so SeqAt::ubase
-// is left 0.)  With
+// position and axis length), and every lane holds the total length C.  With
 // more than 64 sequences the lanes hold the first 64 and positions past them
 // are found by rescanning the table (axis_find).
 struct Axis {
   int P, n;
   int64_t start, len;
+  int ubase;  // index of this lane's sequence's first unit
   int64_t C;
+  int units;  // units of the whole call
 };
 
 // Inclusive prefix sum over the wave.
@@ -848,25 +849,33 @@ __device__ Axis axis_load(const MfmaArgs& a) {
     ax.P = P;
     ax.n = n;
     ax.start = 0;
+    ax.ubase = 0;
     ax.len = lane == 0 ? a.Hkv * c.per_head : 0;
     ax.C = a.Hkv * c.per_head;
+    ax.units = a.Hkv * c.rt;
     return ax;
   }
   int64_t base = 0;
+  int ubase = 0;
   for (int c0 = 0; c0 < a.B; c0 += kWave) {
     int P, n;
     const plan::SeqCost c = lane_cost(a, c0 + lane, &P, &n);
     const int64_t len = c0 + lane < a.B ? a.Hkv * c.per_head : 0;
     const int64_t x = wave_scan_i64(len);
+    const int nu = c0 + lane < a.B ? a.Hkv * c.rt : 0;
+    const int xu = static_cast<int>(wave_scan_i64(nu));
     if (c0 == 0) {
       ax.P = P;
       ax.n = n;
       ax.start = x - len;
       ax.len = len;
+      ax.ubase = xu - nu;
     }
     base += readlane_i64(x, kWave - 1);
+    ubase += __builtin_amdgcn_readlane(xu, kWave - 1);
   }
   ax.C = base;
+  ax.units = ubase;
   return ax;
 }
 
@@ -880,17 +889,22 @@ __device__ plan::SeqAt axis_find(const MfmaArgs& a, const Axis& ax, int64_t p) {
     r.P = __builtin_amdgcn_readlane(ax.P, l);
     r.n = __builtin_amdgcn_readlane(ax.n, l);
     r.pre = readlane_i64(ax.start, l);
+    r.ubase = __builtin_amdgcn_readlane(ax.ubase, l);
     r.c = plan::seq_cost(r.P, r.n, a.G);
     return r;
   }
   // past the first 64 sequences: rescan the table from the second chunk on
   const int lane = __lane_id();
   int64_t base = readlane_i64(ax.start + ax.len, kWave - 1);
+  int ubase = __builtin_amdgcn_readlane(ax.ubase, kWave - 1) +
+              __builtin_amdgcn_readlane(a.Hkv * plan::seq_cost(ax.P, ax.n, a.G).rt, kWave - 1);
   for (int c0 = kWave; c0 < a.B; c0 += kWave) {
     int P, n;
     const plan::SeqCost c = lane_cost(a, c0 + lane, &P, &n);
     const int64_t len = c0 + lane < a.B ? a.Hkv * c.per_head : 0;
     const int64_t x = wave_scan_i64(len);
+    const int nu = c0 + lane < a.B ? a.Hkv * c.rt : 0;
+    const int xu = static_cast<int>(wave_scan_i64(nu));
     const int64_t start = base + x - len;
     const uint64_t h = __ballot(len > 0 && start <= p && p < start + len);
     if (h != 0) {
@@ -899,23 +913,21 @@ __device__ plan::SeqAt axis_find(const MfmaArgs& a, const Axis& ax, int64_t p) {
       r.P = __builtin_amdgcn_readlane(P, l);
       r.n = __builtin_amdgcn_readlane(n, l);
       r.pre = readlane_i64(start, l);
+      r.ubase = ubase + __builtin_amdgcn_readlane(xu - nu, l);
       r.c = plan::seq_cost(r.P, r.n, a.G);
       return r;
     }
     base += readlane_i64(x, kWave - 1);
+    ubase += __builtin_amdgcn_readlane(xu, kWave - 1);
   }
   return r;  // not reached for p < C
 }
 
-// What the merge kernel needs of a unit cut between workgroups: its pieces
-// (plan::MergeJob), written by the attention workgroup that owns the unit's
-// tree block so that the merge workgroups do not redo the partition's
-// arithmetic.  The table has one entry per workgroup: a cut unit's first item
-// lies before the start of its tree block's owner s and its tree block after
-// it, so the unit holds s's first axis position, and no other cut unit has its
-// tree block in s.  Workgroup s marks entry s inactive before it plans and, if
-// it owns such a unit's tree block, writes the unit's descriptor there; the
-// merge grid then has one column per workgroup, nearly all of them busy.
+// What the merge kernel needs of a unit: whether it was cut and, if so, its
+// pieces (plan::MergeJob), written by the attention workgroup that owns the
+// unit's tree block so that the merge workgroups do not redo the partition's
+// arithmetic.  Entry i of the table is the call's unit i; the table's header
+// holds the call's unit count (entries past it are left from other calls).
 struct MergeDesc {
   int32_t active, b, g, rt, n, sa, sa_first, t_pre;
   int64_t U, C;
@@ -1085,7 +1097,8 @@ __global__ void __launch_bounds__(kThreads, 1) attn_stream_kernel(MfmaArgs a) {
       const Axis ax = axis_load(a);
       auto find = [&](int64_t p) { return axis_find(a, ax, p); };
       const plan::Grid gr = plan::make_grid(ax.C, a.W);
-      if (round == 0 && threadIdx.x == 0) a.ws_desc[s].active = 0;  // until a cut unit's tree block
+      if (blockIdx.x == 0 && round == 0 && threadIdx.x == 0)
+        *reinterpret_cast<int32_t*>(a.ws_desc) = ax.units;  // the merge table's header
       bool first = round == 0 ? true : sm.first != 0;
       const int64_t pos = round == 0 ? plan::range_lo(gr, s) : sm.next_pos;
       int k = 0;
@@ -1100,7 +1113,7 @@ __global__ void __launch_bounds__(kThreads, 1) attn_stream_kernel(MfmaArgs a) {
             ++k;
             if (sh.tree) {  // this workgroup owns the unit's last item: its merge entry
               const plan::MergeJob job = plan::unit_job(q, u, U, s, gr, find);
-              if (threadIdx.x == 0 && job.active) {
+              if (threadIdx.x == 0) {
                 MergeDesc d{};
                 d.active = job.active;
                 d.b = q.b;
@@ -1113,7 +1126,7 @@ __global__ void __launch_bounds__(kThreads, 1) attn_stream_kernel(MfmaArgs a) {
                 d.U = U;
                 d.C = ax.C;
                 d.w = u.w;
-                a.ws_desc[s] = d;
+                a.ws_desc[1 + plan::unit_index(q, u)] = d;
               }
             }
           });
@@ -1146,8 +1159,8 @@ __global__ void __launch_bounds__(kThreads, 1) attn_stream_kernel(MfmaArgs a) {
 // Merge of a unit cut between workgroups: out = sum_p w_p * Ohat_p / sum_p w_p,
 // w_p = 2^(m_p - M) * l_p, M = max_p m_p, over the unit's pieces p in
 // workgroup order, where Ohat_p = O_p / l_p is the piece's normalised output
-// (bf16).  blockIdx.x = the merge table's entry (a cut unit, or inactive),
-// blockIdx.y picks 64 of its rows: each wave takes 16 rows, 4 lanes
+// (bf16).  blockIdx.x = the unit (its entry in the merge table says whether it
+// was cut), blockIdx.y picks 64 of its rows: each wave takes 16 rows, 4 lanes
 // per row and a quarter of the head's dims per lane.  Lane k of a wave works out the
 // slot of piece k once (64 pieces per round); every lane then walks the
 // pieces in batches of 4 with all their loads in flight, keeping a running
@@ -1159,8 +1172,9 @@ __global__ void __launch_bounds__(256) attn_stream_merge_kernel(MfmaArgs a) {
   constexpr int kQD = HD / 4;       // dims per lane (4 lanes per row)
   constexpr int kQC = kQD / 8;      // 16-byte chunks per lane
   if (halted(a.status)) return;
-  const MergeDesc d = a.ws_desc[blockIdx.x];
-  if (!d.active) return;
+  const int units = *reinterpret_cast<const int32_t*>(a.ws_desc);
+  const MergeDesc d = a.ws_desc[1 + blockIdx.x];
+  if (static_cast<int>(blockIdx.x) >= units || !d.active) return;
   const int wv = threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   const int rows = min(a.G * d.n - d.rt * kTileRows, kTileRows);
@@ -1409,13 +1423,13 @@ bool mfma_supported(const AttnShape& s) {
 
 int attention_grid(const AttnPlan& p) { return p.mfma ? p.grid : 0; }
 
-// Stream plan: two partial slots per workgroup and the merge table (one entry
-// per workgroup).
+// Stream plan: two partial slots per workgroup and the merge table (a 64-byte
+// header and one entry per unit the call can have).
 void plan_stream(const AttnShape& s, int num_cus, AttnPlan* p) {
   p->mfma = true;
   p->stream = true;
   p->grid = choose_grid(s, num_cus);
-  p->workspace_bytes = static_cast<size_t>(p->grid) * (2 * kSlotBytes + kDescBytes);
+  p->workspace_bytes = 2 * static_cast<size_t>(p->grid) * kSlotBytes + (1 + max_units(s)) * kDescBytes;
 }
 
 void plan_mfma(const AttnShape& s, int num_cus, AttnPlan* p) {
@@ -1482,19 +1496,20 @@ hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q
   a.ws_ml = reinterpret_cast<float*>(ws + slots * kD * 2);
   a.ws_desc = reinterpret_cast<MergeDesc*>(ws + slots * (kD * 2 + 2 * sizeof(float)));
   a.W = p.grid;
+  a.max_units = static_cast<int>(max_units(s));
   if (s.d == 64)
     hipLaunchKernelGGL(attn_stream_kernel<64>, dim3(p.grid), dim3(kThreads), 0, stream, a);
   else
     hipLaunchKernelGGL(attn_stream_kernel<128>, dim3(p.grid), dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // One merge workgroup column per entry of the table, 64 rows per workgroup.
+  // One merge workgroup column per possible unit, 64 rows per workgroup.
   if (s.d == 64)
-    hipLaunchKernelGGL(attn_stream_merge_kernel<64>, dim3(p.grid, kTileRows / 64), dim3(256), 0,
-                       stream, a);
+    hipLaunchKernelGGL(attn_stream_merge_kernel<64>, dim3(a.max_units, kTileRows / 64), dim3(256),
+                       0, stream, a);
   else
-    hipLaunchKernelGGL(attn_stream_merge_kernel<128>, dim3(p.grid, kTileRows / 64), dim3(256), 0,
-                       stream, a);
+    hipLaunchKernelGGL(attn_stream_merge_kernel<128>, dim3(a.max_units, kTileRows / 64), dim3(256),
+                       0, stream, a);
   return hipGetLastError();
 }
 

@@ -84,8 +84,7 @@ def test_bf16_head128_workloads_plan_the_mfma_grid():
         g = ltd.attn_grid(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16, P + Nmax)
         assert g == W, (B, Nmax, Hq, Hkv, P, g)
         assert g == ltd.attn_grid(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16, 16, paged=True)
-        # two partial slots and a 64-byte merge-table entry per workgroup
-        assert ltd.attn_workspace_size(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16) >= g * (2 * slot + 64)
+        assert ltd.attn_workspace_size(B, Nmax, Hq, Hkv, 128, P, ltd.DTYPE_BF16) >= 2 * g * slot
     # blocks so small that a stream share could span more block ids than the
     # LDS table holds: the split plan takes the batch (grid kv heads x row
     # tiles x splits, not a power of two)

@@ -112,7 +112,6 @@ int main() {
     // a cut unit's job lists exactly its pieces' slots, in workgroup order
     std::map<int64_t, int> jobs;
     std::set<int> indices;
-    std::set<int> cut_owners;  // the merge table's entries: one cut unit per tree-block owner
     for (int s = 0; s < W; ++s) {
       bool bad = false;
       for_each_share(s, gr, find, [&](const SeqAt& q, const Unit& u, int64_t U, const Share& sh,
@@ -125,13 +124,6 @@ int main() {
         indices.insert(ui);
         const MergeJob j = unit_job(q, u, U, s, gr, find);
         if (j.active == whole) bad = true;
-        if (j.active) {
-          if (cut_owners.count(s)) bad = true;
-          cut_owners.insert(s);
-          // the cut unit holds the owner's first axis position
-          const int64_t lo = range_lo(gr, s);
-          if (!(U <= lo && lo <= tree_item(U, u.w, q.c.t_pre))) bad = true;
-        }
         std::vector<std::pair<int, int>> got;
         if (j.active)
           for (int k = 0; k <= s - j.sa; ++k) {
