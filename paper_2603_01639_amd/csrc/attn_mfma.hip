@@ -267,7 +267,10 @@ __device__ __forceinline__ LoadPlan make_load_plan(int wave, int lane) {
 // rest the second; a tile never spans both.  With final_out the share is the
 // whole unit and the normalised output goes to `out`; otherwise the share's
 // partial result goes to workspace slot `slot`.
-template <bool kTree, int HD>
+// The cache layout (kPaged) is a compile-time choice, so each kernel's tile
+// loop keeps only its own layout's addressing state in scalar registers (the
+// contiguous instantiation of the split kernel then spills none of them).
+template <bool kTree, int HD, bool kPaged>
 __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g, int row0,
                                        int valid_rows, int key_begin, int n_pre, int P, int n,
                                        bool final_out, int slot) {
@@ -335,7 +338,7 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
   const LoadPlan lp = make_load_plan(wave, lane);
   const unsigned char* kbase = reinterpret_cast<const unsigned char*>(a.k);
   const unsigned char* vbase = reinterpret_cast<const unsigned char*>(a.v);
-  const bool paged = a.block_table != nullptr;
+  constexpr bool paged = kPaged;  // a paged cache (block table) or one contiguous range per (b, g)
   // Paged caches: this split's block ids are staged in LDS first, so address
   // generation never waits on a global load.  The split's rows are one
   // contiguous logical range (for the last split the tree rows follow the
@@ -949,7 +952,7 @@ __device__ __forceinline__ int stream_index(int w, int W) { return (w % 8) * (W 
 // share one XCD (its L2 holds their common Q rows and K/V).  A unit with one
 // split writes its output directly; otherwise split sp leaves its partial in
 // slot (bg * max_splits + sp) * row_tiles + row tile.
-template <int HD>
+template <int HD, bool kPaged>
 __global__ void __launch_bounds__(kThreads, 1) attn_split_kernel(MfmaArgs a) {
   __shared__ __attribute__((aligned(16))) Smem sm;
   const int bg = blockIdx.x;
@@ -971,9 +974,9 @@ __global__ void __launch_bounds__(kThreads, 1) attn_split_kernel(MfmaArgs a) {
   const int n_pre = min(a.split_keys, P - key_begin);
   const int slot = (bg * a.max_splits + split) * a.row_tiles + rtile;
   if (split == nsp - 1)
-    attend<true, HD>(a, sm, b, g, row0, valid_rows, key_begin, n_pre, P, n, nsp == 1, slot);
+    attend<true, HD, kPaged>(a, sm, b, g, row0, valid_rows, key_begin, n_pre, P, n, nsp == 1, slot);
   else
-    attend<false, HD>(a, sm, b, g, row0, valid_rows, key_begin, n_pre, P, n, nsp == 1, slot);
+    attend<false, HD, kPaged>(a, sm, b, g, row0, valid_rows, key_begin, n_pre, P, n, nsp == 1, slot);
 }
 
 // Split plan merge, one wave per stacked row: combine the splits' partials
@@ -1085,7 +1088,7 @@ __global__ void __launch_bounds__(256) attn_split_merge_kernel(MfmaArgs a) {
 // into LDS, then run one by one by the whole workgroup: the partition's state
 // (the sequence table, positions) is dead while the tile loop runs, which
 // keeps it out of the loop's registers.
-template <int HD>
+template <int HD, bool kPaged>
 __global__ void __launch_bounds__(kThreads, 1) attn_stream_kernel(MfmaArgs a) {
   __shared__ __attribute__((aligned(16))) Smem sm;
   if (halted(a.status)) return;
@@ -1145,10 +1148,10 @@ __global__ void __launch_bounds__(kThreads, 1) attn_stream_kernel(MfmaArgs a) {
       const ShareDesc d = sm.share[i];
       const int row0 = d.rt * kTileRows;
       if (d.tree)
-        attend<true, HD>(a, sm, d.b, d.g, row0, a.G * d.n, d.key_begin, d.n_pre, d.P, d.n,
+        attend<true, HD, kPaged>(a, sm, d.b, d.g, row0, a.G * d.n, d.key_begin, d.n_pre, d.P, d.n,
                      d.whole != 0, d.slot);
       else
-        attend<false, HD>(a, sm, d.b, d.g, row0, a.G * d.n, d.key_begin, d.n_pre, d.P, d.n,
+        attend<false, HD, kPaged>(a, sm, d.b, d.g, row0, a.G * d.n, d.key_begin, d.n_pre, d.P, d.n,
                       d.whole != 0, d.slot);
     }
     if (next_pos < 0) break;
@@ -1477,10 +1480,15 @@ hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q
     const size_t slots = static_cast<size_t>(s.B) * s.Hkv * p.max_splits * p.row_tiles * kTileRows;
     a.ws_ml = reinterpret_cast<float*>(ws + slots * kD * 2);
     const dim3 grid(s.B * s.Hkv, p.row_tiles, p.max_splits);
-    if (s.d == 64)
-      hipLaunchKernelGGL(attn_split_kernel<64>, grid, dim3(kThreads), 0, stream, a);
+    const bool paged = a.block_table != nullptr;
+    if (s.d == 64 && paged)
+      hipLaunchKernelGGL((attn_split_kernel<64, true>), grid, dim3(kThreads), 0, stream, a);
+    else if (s.d == 64)
+      hipLaunchKernelGGL((attn_split_kernel<64, false>), grid, dim3(kThreads), 0, stream, a);
+    else if (paged)
+      hipLaunchKernelGGL((attn_split_kernel<128, true>), grid, dim3(kThreads), 0, stream, a);
     else
-      hipLaunchKernelGGL(attn_split_kernel<128>, grid, dim3(kThreads), 0, stream, a);
+      hipLaunchKernelGGL((attn_split_kernel<128, false>), grid, dim3(kThreads), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.max_splits == 1) return e;  // one split: the output is final
     // (sequence, kv head) fastest, as for the attention grid: a head's merge
@@ -1497,10 +1505,15 @@ hipError_t launch_attn_mfma(const AttnShape& s, const AttnPlan& p, const void* q
   a.ws_desc = reinterpret_cast<MergeDesc*>(ws + slots * (kD * 2 + 2 * sizeof(float)));
   a.W = p.grid;
   a.max_units = static_cast<int>(max_units(s));
-  if (s.d == 64)
-    hipLaunchKernelGGL(attn_stream_kernel<64>, dim3(p.grid), dim3(kThreads), 0, stream, a);
+  const bool paged = a.block_table != nullptr;
+  if (s.d == 64 && paged)
+    hipLaunchKernelGGL((attn_stream_kernel<64, true>), dim3(p.grid), dim3(kThreads), 0, stream, a);
+  else if (s.d == 64)
+    hipLaunchKernelGGL((attn_stream_kernel<64, false>), dim3(p.grid), dim3(kThreads), 0, stream, a);
+  else if (paged)
+    hipLaunchKernelGGL((attn_stream_kernel<128, true>), dim3(p.grid), dim3(kThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL(attn_stream_kernel<128>, dim3(p.grid), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL((attn_stream_kernel<128, false>), dim3(p.grid), dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // One merge workgroup column per possible unit, 64 rows per workgroup.
