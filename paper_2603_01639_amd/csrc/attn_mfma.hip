@@ -348,17 +348,19 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     first_blk = key_begin / a.kv_rows;
     const int n_blk = (key_begin + n_pre + n_tree - 1) / a.kv_rows - first_blk + 1;
     const int32_t* bt = a.block_table + static_cast<int64_t>(b) * a.max_blocks + first_blk;
-    for (int j = tid; j < n_blk; j += kThreads) sm.blk[j] = bt[j];
+    // (stored as the block's row group of head g, blk * Hkv + g: its first
+    // row is that times kv_rows)
+    for (int j = tid; j < n_blk; j += kThreads) sm.blk[j] = bt[j] * a.Hkv + g;
     __syncthreads();
   }
   auto row_byte = [&](int row) -> int64_t {  // byte offset of logical cache row `row`
     if (!paged) return ((static_cast<int64_t>(b) * a.Hkv + g) * a.kv_rows + row) * (HD * 2);
     if (a.kv_shift >= 0) {  // power-of-two blocks: shifts and masks, no division
-      const int64_t blk = sm.blk[(row >> a.kv_shift) - first_blk];
-      return (((blk * a.Hkv + g) << a.kv_shift) + (row & (a.kv_rows - 1))) * (HD * 2);
+      const int64_t rg = sm.blk[(row >> a.kv_shift) - first_blk];
+      return ((rg << a.kv_shift) + (row & (a.kv_rows - 1))) * (HD * 2);
     }
-    const int64_t blk = sm.blk[row / a.kv_rows - first_blk];
-    return ((blk * a.Hkv + g) * a.kv_rows + row % a.kv_rows) * (HD * 2);
+    const int64_t rg = sm.blk[row / a.kv_rows - first_blk];
+    return (rg * a.kv_rows + row % a.kv_rows) * (HD * 2);
   };
   // A lane's byte offset of its chunk within a cache row.  The LDS tile keeps
   // 128-dim rows whatever the head size; with 64 dims each row's 8 chunks
@@ -388,6 +390,16 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     k_grp[u] = __builtin_amdgcn_readfirstlane(lp.k_key[u]);
     v_grp[u] = __builtin_amdgcn_readfirstlane(lp.v_key[u]);
   }
+  // For a full prefix tile (rows from a multiple of 64) the block of load u is
+  // the tile's first block plus k_grp[u] >> kv_shift (0 for blocks of 64 rows
+  // or more); a row group's first byte is rg << rg_shift.
+  int k_lix[kKLoads], v_lix[kKLoads];
+#pragma unroll
+  for (int u = 0; u < kKLoads; ++u) {
+    k_lix[u] = a.kv_shift <= 6 ? k_grp[u] >> a.kv_shift : 0;
+    v_lix[u] = a.kv_shift <= 6 ? v_grp[u] >> a.kv_shift : 0;
+  }
+  const int rg_shift = a.kv_shift + (HD == 128 ? 8 : 7);
   // LDS byte addresses of the ring and of this wave's 1 KiB block in a slot,
   // worked out once: a slot's load targets are then scalar adds.
   const uint32_t ring_lds = lds_addr(&sm.kv[0][0]);
@@ -400,20 +412,19 @@ __device__ __forceinline__ void attend(const MfmaArgs& a, Smem& sm, int b, int g
     const TileRef tr = tile_ref(t);
     if (paged_uniform && !tr.tree && tr.left >= kKT && (tr.row & (kKT - 1)) == 0) {
       const int64_t in_row = a.kv_rows > kKT ? static_cast<int64_t>(tr.row & (a.kv_rows - 1)) * (HD * 2) : 0;
+      const int tb = (tr.row >> a.kv_shift) - first_blk;  // the tile's first block
       int bk[kKLoads], bv[kKLoads];
 #pragma unroll
       for (int u = 0; u < kKLoads; ++u) {
-        bk[u] = sm.blk[((tr.row + k_grp[u]) >> a.kv_shift) - first_blk];
-        bv[u] = sm.blk[((tr.row + v_grp[u]) >> a.kv_shift) - first_blk];
+        bk[u] = sm.blk[tb + k_lix[u]];
+        bv[u] = sm.blk[tb + v_lix[u]];
       }
 #pragma unroll
       for (int u = 0; u < kKLoads; ++u) {
-        const int64_t kb = __builtin_amdgcn_readfirstlane(bk[u]);
-        const int64_t vb = __builtin_amdgcn_readfirstlane(bv[u]);
-        dma16(k_lds + pos_lds[u], kbase + (((kb * a.Hkv + g) << a.kv_shift) * (HD * 2) + in_row),
-              k_poff[u]);
-        dma16(v_lds + pos_lds[u], vbase + (((vb * a.Hkv + g) << a.kv_shift) * (HD * 2) + in_row),
-              v_poff[u]);
+        const int64_t kr = __builtin_amdgcn_readfirstlane(bk[u]);
+        const int64_t vr = __builtin_amdgcn_readfirstlane(bv[u]);
+        dma16(k_lds + pos_lds[u], kbase + ((kr << rg_shift) + in_row), k_poff[u]);
+        dma16(v_lds + pos_lds[u], vbase + ((vr << rg_shift) + in_row), v_poff[u]);
       }
     } else if (!paged && tr.left >= kKT) {
       // contiguous rows: a uniform tile base plus per-lane 32-bit offsets
