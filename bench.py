@@ -424,10 +424,12 @@ def workload_key(name, c4_n=None):
 
 
 def attention_by_workload(ltd, torch, to_dev, args, graph_of, timed, stream):
-    """The attention call alone on the other workloads (c4 at depth 6), timed
-    like the main one: a graph of K calls over rotated input copies (> 2x the
-    Infinity Cache, so every call reads cold K/V), replayed once between
-    events on the launch stream."""
+    """The attention call alone on the other workloads (c4 at depth 6): a
+    graph of K calls over rotated input copies (> 2x the Infinity Cache, so
+    every call reads cold K/V), replayed five times between events on the
+    launch stream; the median replay is reported (a single replay of these
+    few-millisecond graphs moves by up to 15% with the clock the chip is at
+    when it starts)."""
     import workloads as W
     out_rows = {}
     steps = max(20, min(args.steps, 100))
@@ -463,7 +465,8 @@ def attention_by_workload(ltd, torch, to_dev, args, graph_of, timed, stream):
         for i in range(3):
             call(i)
         g = graph_of(call, steps)
-        us = 1e3 * timed(lambda i: g.replay(), 1) / steps
+        reps = sorted(timed(lambda i: g.replay(), 1) for _ in range(5))
+        us = 1e3 * reps[len(reps) // 2] / steps
         del g
         key = workload_key(name, n)
         roof = binding_roof("tree_verify_attn", attn_bytes, flops, us)
