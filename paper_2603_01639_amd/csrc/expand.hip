@@ -51,9 +51,6 @@ __device__ __forceinline__ uint32_t orderable(float v) {
 __device__ __forceinline__ float from_orderable(uint32_t o) {
   return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
 }
-__device__ __forceinline__ uint64_t pack(float v, uint32_t idx) {
-  return (static_cast<uint64_t>(orderable(v)) << 32) | (0xFFFFFFFFu - idx);
-}
 __device__ __forceinline__ uint32_t key_index(uint64_t k) {
   return 0xFFFFFFFFu - static_cast<uint32_t>(k);
 }
