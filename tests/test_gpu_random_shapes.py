@@ -43,7 +43,7 @@ def _case(seed):
             break
         B = max(1, B - 1)
     trees = [_tree(rng, n) for n in ns]
-    Nmax = max(ns) + int(rng.integers(0, 3))
+    Nmax = min(256, max(ns) + int(rng.integers(0, 3)))  # the ABI takes at most 256 nodes
     Voc = int(rng.choice([257, 3000]))
     toks = [W.distinct_sibling_tokens(rng, t, Voc) for t in trees]
     label = (f"random seed={seed} dtype={dtype} d={d} Hkv={Hkv} G={G} B={B} block={block} "
