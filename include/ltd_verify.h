@@ -219,7 +219,9 @@ int ltd_tree_accept_noalloc(const float* logits, const int32_t* draft_tokens,
  *   workspace: ltd_tree_accept_sampling_workspace_size(B, Nmax, Voc) bytes.
  * Decisions are taken on float32 element arithmetic with double sums, so they
  * can differ from an exact evaluation only where a uniform lies within about
- * 1e-6 (relative) of its threshold.
+ * 1e-6 (relative) of its threshold.  The draft mass left after each rejection
+ * is summed over the tokens not rejected, so it stays exact to double
+ * rounding however little of it is left.
  */
 size_t ltd_tree_accept_sampling_workspace_size(int B, int Nmax, int Voc);
 

@@ -7,14 +7,22 @@
 //
 // The residuals never need to be stored.  Children carry distinct tokens, and
 // after k rejections at a node every token v has
-//     P_k(v) = max(P(v) - g_k Q(v), 0) / s_k,   Q_k(v) = Q(v) / (1 - D_k)
-// (a rejected token's residual is already 0), with g_1 = 0, s_1 = 1, D_1 = 0
-// and, on the k-th rejection of token x,
-//     g_{k+1} = g_k + s_k / (1 - D_k),  D_{k+1} = D_k + Q(x),
-//     s_{k+1} = sum_v max(P(v) - g_{k+1} Q(v), 0)   (kept if it is 0).
-// So an accept test needs only P(x) and Q(x) and two scalars, each rejection
-// one pass over the vocabulary for s_{k+1}, and the bonus one inverse-CDF pass.
-// None of g_k, s_k, D_k depends on the uniforms: a node's children are tried in
+//     P_k(v) = max(P(v) - g_k Q(v), 0) / s_k,   Q_k(v) = Q(v) / R_k
+// for tokens not yet rejected (a rejected token's residual is already 0 and
+// its Q_k is 0), with g_1 = 0, s_1 = 1, R_1 = 1 and, on the k-th rejection,
+//     g_{k+1} = g_k + s_k / R_k,
+//     s_{k+1} = sum_v max(P(v) - g_{k+1} Q(v), 0)   (kept if it is 0),
+//     R_{k+1} = sum of Q(v) over the tokens not rejected so far.
+// R is summed over the remaining tokens, never taken as 1 minus the rejected
+// mass: when the rejected drafts hold nearly all of Q that difference loses
+// every digit (a draft row of 0.9998 on one token leaves 2e-4, and a few more
+// rejections leave less than double rounding of 1), and g with it.  Once R is
+// 0 (every token with draft mass rejected) Q_k is 0: a child is accepted
+// where P_k(x) > 0 and a rejection leaves P as it is.
+// So an accept test needs only P(x) and Q(x) and three scalars, each rejection
+// one pass over the vocabulary for s_{k+1} and R_{k+1}, and the bonus one
+// inverse-CDF pass.
+// None of g_k, s_k, R_k depends on the uniforms: a node's children are tried in
 // a fixed order, so the residual after its k-th rejection is the same whatever
 // the draws, and its mass can be taken for every node at once, before the
 // walk, one level k per launch (level k needs the total of level k - 1).  The
@@ -28,11 +36,13 @@
 //                        nodes with at least k children only: per chunk, the
 //                        residual mass after the node's k-th rejection, with
 //                        the walk's own parameters and arithmetic (the mass at
-//                        g = 0 is the chunk's softmax partial);
+//                        g = 0 is the chunk's softmax partial), and the
+//                        chunk's draft mass outside the rejected tokens;
 //   sample_walk_kernel   one 1024-thread workgroup per sequence walks the tree:
 //                        scalar accept tests; a node's first kLevels rejections
 //                        read their masses from the tables, each later one
-//                        takes a block-wide pass; the bonus takes its chunk from
+//                        takes a block-wide pass (the rejected tokens are bits
+//                        of an LDS bitmap of the vocabulary); the bonus takes its chunk from
 //                        a table when its residual is one of them, and
 //                        otherwise narrows the range holding the target mass
 //                        sixteenfold per level (one coalesced segment sum per
@@ -56,23 +66,34 @@ static_assert(kMaxChunks <= kWave, "the walk merges one chunk partial a lane");
 constexpr int kLevels = 3;  // rejections per node whose residual masses are tabled
 
 // The residual after a node's rejections so far: P_k = max(P - g Q, 0) / s,
-// and D = the draft mass of the rejected tokens.  The walk and the mass
+// and R = the draft mass of the tokens not rejected.  The walk and the mass
 // tables advance it with the same operations, so both see bit-identical g.
 struct RejState {
-  double g, s, D;
+  double g, s, R;
 };
-// g of the residual after the next rejection.
-__device__ __forceinline__ double next_g(const RejState& st) { return st.g + st.s / (1.0 - st.D); }
-// The rejection of a token with draft probability Qx (counted once even if the
-// token was rejected before), after which the residual at g2 has mass s2 (a
-// residual without mass leaves P as it was).
-__device__ __forceinline__ void reject(RejState& st, double g2, double s2, double Qx, bool repeat) {
-  if (!repeat) st.D += Qx;
+// g of the residual after the next rejection (unchanged once no draft mass
+// is left: Q_k is then 0 and a rejection leaves P as it is).
+__device__ __forceinline__ double next_g(const RejState& st) {
+  return st.R > 0.0 ? st.g + st.s / st.R : st.g;
+}
+// The rejection after which the residual at g2 has mass s2 and R2 of the
+// draft mass is left (a residual without mass leaves P as it was).
+__device__ __forceinline__ void reject(RejState& st, double g2, double s2, double R2) {
+  st.R = R2;
   if (s2 > 0.0) {
     st.g = g2;
     st.s = s2;
   }
 }
+// The draft mass left, R = (draft sum outside the rejected tokens) / QS.
+__device__ __forceinline__ double left_mass(double keep, double QS) {
+  return QS > 0.0 ? keep / QS : 1.0;
+}
+// One entry of a mass table, per (level, sequence, node, chunk).
+struct MassEntry {
+  double mass;  // the chunk's residual mass after the level-th rejection
+  double keep;  // the chunk's draft sum outside the first `level` children's tokens
+};
 
 // Node j's parent as every kernel here reads it: in [0, j - 1] (the links of
 // a valid tree; malformed ones are clamped, so all kernels agree on the tree).
@@ -86,6 +107,25 @@ struct NodeStats {  // per (sequence, node, chunk)
   float qs;  // sum of the draft row over the chunk (nodes with children)
   float pad;
 };
+
+// Wave-wide double sum (every lane gets it).
+__device__ __forceinline__ double wave_sum_d(double v, int lane) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) {
+    uint64_t o;
+    const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(v));
+    switch (d) {
+      case 32: o = lane_xor_u64<32>(bits, lane); break;
+      case 16: o = lane_xor_u64<16>(bits, lane); break;
+      case 8: o = lane_xor_u64<8>(bits, lane); break;
+      case 4: o = lane_xor_u64<4>(bits, lane); break;
+      case 2: o = lane_xor_u64<2>(bits, lane); break;
+      default: o = lane_xor_u64<1>(bits, lane);
+    }
+    v += __longlong_as_double(static_cast<long long>(o));
+  }
+  return v;
+}
 
 __global__ void __launch_bounds__(kStatThreads) sample_stats_kernel(
     const float* __restrict__ logits, const float* __restrict__ draft_probs,
@@ -174,13 +214,18 @@ __device__ __forceinline__ float residual_elem(float l, float q, const Residual&
   return fmaxf(fmaf(-r.gq, q, p), 0.f);
 }
 
-// One thread's share of sum_v R(v): float4 loads of both rows in batches of
-// kBatch, all issued before any use (a strided, coalesced layout; rows of a
+// Whether token v is marked in the rejected-token bitmap.
+__device__ __forceinline__ bool marked(const uint32_t* bm, int v) { return (bm[v >> 5] >> (v & 31)) & 1u; }
+
+// One thread's share of sum_v R(v), and in `keep` of the draft sum over the
+// tokens not marked in `bm`: float4 loads of both rows in batches of kBatch,
+// all issued before any use (a strided, coalesced layout; rows of a
 // vocabulary that is not a multiple of 4 take the scalar path).
 constexpr int kBatch = 4;
 __device__ float residual_pass(const float* __restrict__ l, const float* __restrict__ q, int Voc,
-                               int t, const Residual& r) {
+                               int t, const Residual& r, const uint32_t* bm, double& keep) {
   float part = 0.f;
+  keep = 0.0;
   const bool aligned = (Voc & 3) == 0 && (reinterpret_cast<uintptr_t>(l) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(q) & 15) == 0;
   if (aligned) {
@@ -197,11 +242,17 @@ __device__ float residual_pass(const float* __restrict__ l, const float* __restr
       }
 #pragma unroll
       for (int k = 0; k < kBatch; ++k) {
-        if (i0 + k * kWalkThreads < n4) {
+        const int i = i0 + k * kWalkThreads;
+        if (i < n4) {
           part += residual_elem(lv[k].x, qv[k].x, r);
           part += residual_elem(lv[k].y, qv[k].y, r);
           part += residual_elem(lv[k].z, qv[k].z, r);
           part += residual_elem(lv[k].w, qv[k].w, r);
+          const uint32_t bits = bm[i >> 3] >> (4 * (i & 7));  // tokens 4i .. 4i+3
+          keep += (bits & 1u) ? 0.0 : static_cast<double>(qv[k].x);
+          keep += (bits & 2u) ? 0.0 : static_cast<double>(qv[k].y);
+          keep += (bits & 4u) ? 0.0 : static_cast<double>(qv[k].z);
+          keep += (bits & 8u) ? 0.0 : static_cast<double>(qv[k].w);
         }
       }
     }
@@ -215,9 +266,13 @@ __device__ float residual_pass(const float* __restrict__ l, const float* __restr
         qv[k] = q[v];
       }
 #pragma unroll
-      for (int k = 0; k < kBatch; ++k)
-        if (v0 + k * kWalkThreads < Voc)
+      for (int k = 0; k < kBatch; ++k) {
+        const int v = v0 + k * kWalkThreads;
+        if (v < Voc) {
           part += residual_elem(lv[k], qv[k], r);
+          keep += marked(bm, v) ? 0.0 : static_cast<double>(qv[k]);
+        }
+      }
     }
   }
   return part;
@@ -273,25 +328,6 @@ __device__ __forceinline__ Residual residual_params(const NodeTotals& nt, float 
                                       static_cast<double>(__logf(static_cast<float>(nt.Z)))));
   r.gq = g > 0.0 && nt.QS > 0.0 ? static_cast<float>(g / nt.QS) : 0.f;
   return r;
-}
-
-// Wave-wide double sum (every lane gets it).
-__device__ __forceinline__ double wave_sum_d(double v, int lane) {
-#pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) {
-    uint64_t o;
-    const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(v));
-    switch (d) {
-      case 32: o = lane_xor_u64<32>(bits, lane); break;
-      case 16: o = lane_xor_u64<16>(bits, lane); break;
-      case 8: o = lane_xor_u64<8>(bits, lane); break;
-      case 4: o = lane_xor_u64<4>(bits, lane); break;
-      case 2: o = lane_xor_u64<2>(bits, lane); break;
-      default: o = lane_xor_u64<1>(bits, lane);
-    }
-    v += __longlong_as_double(static_cast<long long>(o));
-  }
-  return v;
 }
 
 // Block-wide double sum of one value per thread (every thread gets it).
@@ -362,8 +398,8 @@ __global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
     const float* __restrict__ logits, const float* __restrict__ draft_probs,
     const int32_t* __restrict__ draft_tokens, const int32_t* __restrict__ parents,
     const int32_t* __restrict__ n_nodes, int Nmax, int Voc, float inv_t,
-    const NodeStats* __restrict__ ws, double* __restrict__ mass, int level, int64_t level_stride,
-    const int32_t* status) {
+    const NodeStats* __restrict__ ws, MassEntry* __restrict__ mass, int level,
+    int64_t level_stride, const int32_t* status) {
   static_assert(kStatThreads >= LTD_MAX_NODES, "one thread per node for the child bits");
   __shared__ NodeTotals nt_s;
   __shared__ uint64_t kids_s[kStatThreads / kWave];
@@ -371,6 +407,7 @@ __global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
   __shared__ int ctok_s[LTD_MAX_NODES];  // tokens of the node's children
   __shared__ double g_s;
   __shared__ double red_s[kStatThreads / kWave];
+  __shared__ double keep_s[kStatThreads / kWave];
   if (halted(status)) return;
   const int chunk = blockIdx.x, i = blockIdx.y, b = blockIdx.z;
   const int chunks = gridDim.x;
@@ -379,7 +416,7 @@ __global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
   if (i >= n) return;  // uniform for the block
   const int64_t nb = static_cast<int64_t>(b) * Nmax;
   const int64_t row = (nb + i) * Voc;
-  double* out = mass + (level - 1) * level_stride + (nb + i) * chunks + chunk;
+  MassEntry* out = mass + (level - 1) * level_stride + (nb + i) * chunks + chunk;
   {  // the node's children as bits, thread j for node j, and their tokens
     const bool kid = t < n && t > i && link(parents, nb, t) == i;
     const int tok = min(max(draft_tokens[nb + min(t, n - 1)], 0), Voc - 1);
@@ -396,7 +433,7 @@ __global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
 #pragma unroll
   for (int word = 0; word < kStatThreads / kWave; ++word) n_kids += __popcll(kids_s[word]);
   if (n_kids < level) {  // uniform: the node never rejects `level` times
-    if (t == 0) *out = 0.0;
+    if (t == 0) *out = MassEntry{0.0, 0.0};
     return;
   }
   if (t == 0) {  // its first `level` children's tokens, in ascending order
@@ -414,16 +451,16 @@ __global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
   const NodeTotals nt = nt_s;
   // wave 0's loads for the replay first, then every thread's share of the
   // chunk's rows, in flight while the residual's g is worked out
-  double prev_mass[kLevels - 1], prev_q[kLevels - 1];
+  double prev_mass[kLevels - 1], prev_keep[kLevels - 1];
   if (w == 0) {
 #pragma unroll
     for (int k = 0; k < kLevels - 1; ++k) {
       prev_mass[k] = 0.0;
-      prev_q[k] = 0.0;
-      if (k < level - 1) {
-        const double* prev = mass + k * level_stride + (nb + i) * chunks;
-        prev_mass[k] = lane < chunks ? prev[lane] : 0.0;
-        prev_q[k] = static_cast<double>(draft_probs[row + tok_s[k]]);
+      prev_keep[k] = 0.0;
+      if (k < level - 1 && lane < chunks) {
+        const MassEntry e = mass[k * level_stride + (nb + i) * chunks + lane];
+        prev_mass[k] = e.mass;
+        prev_keep[k] = e.keep;
       }
     }
   }
@@ -436,34 +473,54 @@ __global__ void __launch_bounds__(kStatThreads) sample_mass_kernel(
     q[k] = draft_probs[v];
   }
   if (w == 0) {  // g after `level` rejections: the walk's state, replayed
-    RejState st{0.0, 1.0, 0.0};
+    RejState st{0.0, 1.0, 1.0};
 #pragma unroll
     for (int k = 0; k < kLevels - 1; ++k) {
       if (k < level - 1) {
         const double tot = wave_sum_d(prev_mass[k], lane);
-        const double Qx = nt.QS > 0.0 ? prev_q[k] / nt.QS : 0.0;
-        bool repeat = false;
-        for (int j = 0; j < k; ++j) repeat = repeat || tok_s[j] == tok_s[k];
+        const double keep = wave_sum_d(prev_keep[k], lane);
         const double g2 = next_g(st);
-        reject(st, g2, tot, Qx, repeat);
+        reject(st, g2, tot, left_mass(keep, nt.QS));
       }
     }
     if (lane == 0) g_s = next_g(st);
   }
   __syncthreads();
   const Residual r = residual_params(nt, inv_t, g_s);
-  double d = 0.0;
+  // The draft sum outside the first `level` children's tokens: a sum of
+  // non-negative terms, so float partials keep it to a relative error, however
+  // small it is (the difference it replaces would lose every digit).
+  int ex[kLevels];
 #pragma unroll
-  for (int k = 0; k < kPerThread; ++k)
-    if (base + k * kStatThreads + t < Voc) d += static_cast<double>(residual_elem(l[k], q[k], r));
+  for (int j = 0; j < kLevels; ++j) ex[j] = j < level ? tok_s[j] : -1;
+  double d = 0.0;
+  float kf = 0.f;
+#pragma unroll
+  for (int k = 0; k < kPerThread; ++k) {
+    const int v = base + k * kStatThreads + t;
+    if (v < Voc) {
+      d += static_cast<double>(residual_elem(l[k], q[k], r));
+      bool gone = false;
+#pragma unroll
+      for (int j = 0; j < kLevels; ++j) gone = gone || ex[j] == v;
+      kf += gone ? 0.f : q[k];
+    }
+  }
   d = wave_sum_d(d, lane);
-  if (lane == 0) red_s[w] = d;
+  const double kp = static_cast<double>(wave_sum(kf));
+  if (lane == 0) {
+    red_s[w] = d;
+    keep_s[w] = kp;
+  }
   __syncthreads();
   if (t == 0) {
-    double a = 0.0;
+    double a = 0.0, kk = 0.0;
 #pragma unroll
-    for (int k = 0; k < kStatThreads / kWave; ++k) a += red_s[k];
-    *out = a;
+    for (int k = 0; k < kStatThreads / kWave; ++k) {
+      a += red_s[k];
+      kk += keep_s[k];
+    }
+    *out = MassEntry{a, kk};
   }
 }
 
@@ -480,13 +537,15 @@ __device__ __forceinline__ bool child_any(const int32_t* par_s, int n, int u, in
 // tables').  0 for rejections the node cannot have.  The loads and the merge
 // are separate steps, so a wave can have a node's loads in flight while it
 // works on something else.
-constexpr int kNodeVals = 3 + kLevels;
+// node_out: [0] M, [1] Z, [2] QS, [3 + k] the residual mass after the node's
+// (k+1)-th rejection, [3 + kLevels + k] the draft sum left after it.
+constexpr int kNodeVals = 3 + 2 * kLevels;
 struct NodeLoads {
   NodeStats st;
-  double mk[kLevels];
+  MassEntry mk[kLevels];
 };
 __device__ __forceinline__ NodeLoads node_loads(const NodeStats* __restrict__ ws,
-                                                const double* __restrict__ mass,
+                                                const MassEntry* __restrict__ mass,
                                                 int64_t level_stride, int64_t nb, int v, int chunks,
                                                 int lane) {
   NodeLoads r;
@@ -504,19 +563,24 @@ __device__ void node_merge(const NodeLoads& ld, const int32_t* par_s, int n, int
   const double m0c =
       st.m != -INFINITY ? static_cast<double>(st.z * __expf(st.m - nt.Mf)) / nt.Z : 0.0;
   if (lane < chunks) mass_out[lane][0] = m0c;
-  double tot[kLevels];
+  double tot[kLevels], keep[kLevels];
 #pragma unroll
   for (int k = 0; k < kLevels; ++k) {
-    const double mc = kids ? ld.mk[k] : 0.0;
+    const double mc = kids ? ld.mk[k].mass : 0.0;
+    const double kc = kids ? ld.mk[k].keep : 0.0;
     if (lane < chunks) mass_out[lane][k + 1] = mc;
     tot[k] = wave_sum_d(lane < chunks ? mc : 0.0, lane);
+    keep[k] = wave_sum_d(lane < chunks ? kc : 0.0, lane);
   }
   if (lane == 0) {
     node_out[0] = nt.Mf;
     node_out[1] = nt.Z;
     node_out[2] = nt.QS;
 #pragma unroll
-    for (int k = 0; k < kLevels; ++k) node_out[3 + k] = tot[k];
+    for (int k = 0; k < kLevels; ++k) {
+      node_out[3 + k] = tot[k];
+      node_out[3 + kLevels + k] = keep[k];
+    }
   }
 }
 
@@ -524,7 +588,7 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
     const float* __restrict__ logits, const float* __restrict__ draft_probs,
     const int32_t* __restrict__ draft_tokens, const int32_t* __restrict__ parents,
     const int32_t* __restrict__ n_nodes, const float* __restrict__ uniforms, int Nmax, int Voc,
-    float inv_t, const NodeStats* __restrict__ ws, const double* __restrict__ mass,
+    float inv_t, const NodeStats* __restrict__ ws, const MassEntry* __restrict__ mass,
     int64_t level_stride, int chunks, int32_t* __restrict__ accepted,
     int32_t* __restrict__ out_tokens, int32_t* __restrict__ n_accepted, const int32_t* status) {
   __shared__ int32_t par_s[LTD_MAX_NODES];
@@ -541,9 +605,12 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
   __shared__ double target_s;  // the bonus search: mass left to pass in [lo_s, hi_s)
   __shared__ double seg_s[kWave];  // the bonus search's segment sums
   __shared__ int lo_s, hi_s;
+  // The rejected tokens of the current node, one bit per vocabulary entry.
+  __shared__ uint32_t gone_s[LTD_SAMPLING_MAX_CHUNKS * kChunk / 32];
   if (halted(status)) return;
   const int b = blockIdx.x;
   const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  for (int k = t; k < (Voc + 31) / 32; k += kWalkThreads) gone_s[k] = 0u;
   const int n = min(max(n_nodes[b], 1), Nmax);
   const int64_t nb = static_cast<int64_t>(b) * Nmax;
   if (t < Nmax) {
@@ -590,7 +657,7 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
     const double inv_z = 1.0 / Z;
     Residual res = residual_params(nt, inv_t, 0.0);
 
-    RejState st{0.0, 1.0, 0.0};  // the residual after the rejections so far
+    RejState st{0.0, 1.0, 1.0};  // the residual after the rejections so far
     int lvl = 0;                 // the mass table holding that residual (-1: none)
     int n_removed = 0;
     int next = -1;
@@ -606,11 +673,12 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
         const double Qx = QS > 0.0 ? static_cast<double>(cq_s[c]) / QS : 0.0;
         bool removed = false;
         for (int k = 0; k < n_removed; ++k) removed = removed || removed_s[k] == x;
-        // accept when r Q_k(x) < P_k(x), i.e. r Q(x) s < max(P(x) - g Q(x), 0) (1 - D)
-        // (Q_k(x) = 0 for a token rejected before)
+        // accept when r Q_k(x) < P_k(x), i.e. r Q(x) s < max(P(x) - g Q(x), 0) R
+        // (Q_k(x) = 0 for a token rejected before, and for every token once
+        // R = 0)
         const double Pres = fmax(Px - st.g * Qx, 0.0);
         const double r = static_cast<double>(cr_s[c]);
-        const bool accept = removed ? Pres > 0.0 : r * Qx * st.s < Pres * (1.0 - st.D);
+        const bool accept = removed || st.R <= 0.0 ? Pres > 0.0 : r * Qx * st.s < Pres * st.R;
         if (accept) {
           next = c;
           break;
@@ -618,26 +686,35 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
         // rejected: the next residual's mass, from the tables for the
         // node's first kLevels rejections, else one pass over the vocabulary
         const double g2 = next_g(st);
-        double s2;
+        double s2, R2;
+        if (t == 0) gone_s[x >> 5] |= 1u << (x & 31);
         if (n_removed < kLevels) {
           s2 = node_s[0][3 + n_removed];
+          R2 = left_mass(node_s[0][3 + kLevels + n_removed], QS);
         } else {
           res = residual_params(nt, inv_t, g2);
-          const float part = residual_pass(logits + row, draft_probs + row, Voc, t, res);
+          __syncthreads();  // x's bit
+          double keep;
+          const float part =
+              residual_pass(logits + row, draft_probs + row, Voc, t, res, gone_s, keep);
           s2 = block_sum(static_cast<double>(part), red_s, lane, w);
+          R2 = left_mass(block_sum(keep, red_s, lane, w), QS);
         }
         // (every thread keeps the list, with the same values: no barrier)
         removed_s[n_removed] = x;
-        reject(st, g2, s2, Qx, removed);
+        reject(st, g2, s2, R2);
         if (s2 > 0.0) lvl = n_removed < kLevels ? n_removed + 1 : -1;
         ++n_removed;
       }
     }
     if (next >= 0) {
-      if (t == 0) path_s[len] = next;
+      if (t == 0) {
+        path_s[len] = next;
+        for (int k = 0; k < n_removed; ++k) gone_s[removed_s[k] >> 5] = 0u;  // the new node's start
+      }
       ++len;
       u = next;
-      __syncthreads();  // the node's data and child_s are rewritten for the new node
+      __syncthreads();  // the node's data, child_s and the bitmap are rewritten for the new node
       continue;
     }
 
@@ -843,7 +920,7 @@ __global__ void __launch_bounds__(kWalkThreads) sample_walk_kernel(
 int sampling_chunks(int Voc) { return (Voc + kChunk - 1) / kChunk; }
 
 size_t sampling_workspace_bytes(int B, int Nmax, int Voc) {
-  return (sizeof(NodeStats) + kLevels * sizeof(double)) * static_cast<size_t>(B) * Nmax *
+  return (sizeof(NodeStats) + kLevels * sizeof(MassEntry)) * static_cast<size_t>(B) * Nmax *
          sampling_chunks(Voc);
 }
 
@@ -854,9 +931,9 @@ hipError_t launch_sampling(const float* logits, const float* draft_probs,
                            int32_t* out_tokens, int32_t* n_accepted, void* workspace,
                            const int32_t* status, hipStream_t stream) {
   const int chunks = sampling_chunks(Voc);
-  const int64_t level_stride = static_cast<int64_t>(B) * Nmax * chunks;  // doubles per table
+  const int64_t level_stride = static_cast<int64_t>(B) * Nmax * chunks;  // entries per table
   auto* ws = static_cast<NodeStats*>(workspace);
-  auto* mass = reinterpret_cast<double*>(ws + level_stride);
+  auto* mass = reinterpret_cast<MassEntry*>(ws + level_stride);
   const float inv_t = 1.0f / temperature;
   hipLaunchKernelGGL(sample_stats_kernel, dim3(chunks, Nmax, B), dim3(kStatThreads), 0, stream,
                      logits, draft_probs, parents, n_nodes, Nmax, Voc, inv_t, ws, status);

@@ -183,4 +183,4 @@ def test_sampling_rejects_bad_scalar_arguments(args):
 def test_sampling_workspace():
     # per node and 4096-token chunk: a softmax partial (16 bytes) and the
     # residual masses after the node's first three rejections (doubles)
-    assert ltd.accept_sampling_workspace_size(1, 60, 128256) == 60 * 32 * (16 + 3 * 8)
+    assert ltd.accept_sampling_workspace_size(1, 60, 128256) == 60 * 32 * (16 + 3 * 16)

@@ -94,6 +94,20 @@ def test_batches_of_trees(T, noise, Voc):
             assert acc[b, 1:n[b]].tolist() == depth_path
 
 
+def test_rejections_that_exhaust_the_draft_mass():
+    """Peaked drafts (noise 8) at T = 0.3 over stars of 120 to 256 children:
+    after a few rejections the rejected drafts hold all but a sliver of the
+    draft mass, and after a few more all but less than double rounding of 1.
+    The remaining mass must be summed over the tokens left; taken as 1 minus
+    the rejected mass it loses every digit, and the walk then accepted
+    children the rule rejects."""
+    for seed in range(2):
+        rng = W.rng_for(4242 + seed)
+        trees = [W.tree_star(n) for n in (200, 150, 120, 256)]
+        _check(W.make_sampling_batch(rng, trees, 4097, temperature=0.3, draft_noise=8.0,
+                                     label=f"exhausted draft mass {seed}"))
+
+
 def test_losslessness_on_the_gpu():
     """The property the rule exists for, measured on the kernel alone: 40000
     toy verifications; the first emitted token follows the root's target and
